@@ -1,0 +1,184 @@
+"""Pins of the oracle's decision rules and gated block decode (Eqs. 2-4, termination).
+
+Against: a hand-worked decode (tests/golden/worked_example.json), invariants the
+paper states (U shrinks by exactly T and A, committed tokens never change, the
+gate acts only on positions the transfer rule leaves, dense recovery with the
+gate off), and special cases with known pass counts.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+
+from oracle import decode, theory
+
+
+def test_persistence_counter_scripted():
+    """Eq. (2): counter zero at the first executed step, +1 per repeated top-1, reset on change."""
+    seq = [5, 5, 7, 7, 7, 2, 2]
+    want = [0, 1, 0, 1, 2, 0, 1]
+    prev, m = np.array([decode.NONE]), np.array([0])
+    got = []
+    for x in seq:
+        prev, m = decode.persistence_update(prev, m, np.array([x]))
+        got.append(int(m[0]))
+    assert got == want
+
+
+def test_transfer_schedule():
+    assert decode.transfer_schedule(32, 16).tolist() == [2] * 16
+    assert decode.transfer_schedule(32, 32).tolist() == [1] * 32
+    assert decode.transfer_schedule(10, 4).tolist() == [3, 3, 2, 2]
+    for M in range(1, 40):
+        for S in range(1, M + 1):
+            k = decode.transfer_schedule(M, S)
+            assert k.sum() == M and k.max() - k.min() <= 1 and (np.diff(k) <= 0).all()
+
+
+def test_transfer_set_ties_and_clipping():
+    c32 = np.zeros(10, np.float32)
+    c32[[2, 5, 7]] = [0.5, 0.9, 0.5]
+    assert decode.transfer_set([2, 5, 7], c32, 1).tolist() == [5]
+    assert decode.transfer_set([2, 5, 7], c32, 2).tolist() == [2, 5]     # tie 2 vs 7 -> 2
+    assert decode.transfer_set([2, 5, 7], c32, 9).tolist() == [2, 5, 7]
+    assert decode.transfer_set([], c32, 3).tolist() == []
+
+
+def test_gate_inclusive_boundaries():
+    c = np.array([0.5, 0.5, np.nextafter(np.float32(0.5), np.float32(0))], np.float32)
+    m = np.array([1, 0, 1])
+    assert decode.gate_accept(c, m, 0.5, 1).tolist() == [True, False, False]
+    assert decode.gate_accept(c, m, 0.5, 0).tolist() == [True, True, False]
+
+
+def _scripted_logits_fn(script, V):
+    calls = {"n": 0}
+
+    def fn(tokens, rows):
+        s = calls["n"]
+        calls["n"] += 1
+        out = []
+        for b, r in enumerate(rows):
+            l = np.zeros((len(r), V))
+            for j, p in enumerate(r):
+                if str(int(p)) in script[s]:
+                    l[j] = script[s][str(int(p))]
+            out.append(l)
+        return out
+    return fn
+
+
+def test_worked_example(golden_dir):
+    with open(os.path.join(golden_dir, "worked_example.json")) as f:
+        ex = json.load(f)
+    for case in ex["cases"]:
+        fn = _scripted_logits_fn(ex["script"], ex["vocab"])
+        tokens, passes, trace = decode.block_decode(
+            fn, np.array(ex["prompt"]), ex["gen_len"], ex["mask_id"], ex["block_len"],
+            ex["steps_per_block"], case["delta_p"], case["m_req"], case["gate_enabled"],
+            record=True)
+        assert tokens.tolist() == case["tokens"], case["name"]
+        assert passes.tolist() == case["passes"], case["name"]
+        for want, step in zip(case["per_step"], trace):
+            out = step["out"][0]
+            assert out["T"].tolist() == want["T"], case["name"]
+            assert out["A"].tolist() == want["A"], case["name"]
+
+
+class _RandomModel:
+    """Deterministic stand-in backbone: logits are a fixed random function of the canvas,
+    so earlier commits change later predictions (accepted tokens stay visible)."""
+
+    def __init__(self, V, L, seed, scale):
+        rng = np.random.default_rng(seed)
+        self.E = rng.normal(0, 1, (V, 16))
+        self.P = rng.normal(0, 1, (L, 16))
+        self.W = rng.normal(0, 1, (16, V)) * scale
+        self.V = V
+
+    def __call__(self, tokens, rows):
+        out = []
+        for b, r in enumerate(rows):
+            ctx = np.tanh(self.E[tokens[b]].mean(0))
+            h = self.P[np.asarray(r)] + ctx
+            out.append(h @ self.W)
+        return out
+
+
+@pytest.mark.parametrize("seed", range(6))
+@pytest.mark.parametrize("delta_p,m_req,gate", [(0.65, 1, True), (0.3, 0, True), (0.5, 2, True),
+                                                 (0.65, 1, False)])
+def test_decode_invariants(seed, delta_p, m_req, gate):
+    V, P, G, blk, S = 23, 5, 24, 8, 4
+    mask_id = V - 1
+    model = _RandomModel(V, P + G, seed, scale=1.5)
+    prompt = np.random.default_rng(100 + seed).integers(0, V - 1, (2, P))
+    tokens, passes, trace = decode.block_decode(model, prompt, G, mask_id, blk, S, delta_p,
+                                                m_req, gate, record=True)
+    ks = decode.transfer_schedule(blk, S)
+    for step in trace:
+        pre = step["pre"]
+        for b, out in step["out"].items():
+            lo = P + out["block"] * blk
+            pos = np.arange(lo, lo + blk)
+            U_blk = pos[pre["unresolved"][b, pos] == 1]
+            T, A = out["T"], out["A"]
+            assert len(np.intersect1d(T, A)) == 0                  # gate only on U \ T
+            assert set(T) <= set(U_blk) and set(A) <= set(U_blk)   # only the active block
+            assert len(T) == min(ks[out["step"]], len(U_blk))      # exactly k_s fixed
+            for i in A:                                            # Eq. (3)
+                assert out["c32"][i - lo] >= np.float32(delta_p) and out["m"][i] >= m_req
+            if not gate:
+                assert len(A) == 0
+            # T holds the highest confidences of U_blk
+            if len(T) and len(U_blk) > len(T):
+                rest = np.setdiff1d(U_blk, T)
+                assert out["c32"][T - lo].min() >= out["c32"][rest - lo].max()
+    # Eq. (4): U shrinks by exactly T and A, committed tokens never change afterwards
+    for s0, s1 in zip(trace[:-1], trace[1:]):
+        for b, out in s0["out"].items():
+            fixed = np.union1d(out["T"], out["A"])
+            before, after = s0["pre"]["unresolved"][b], s1["pre"]["unresolved"][b]
+            assert (before.astype(int) - after.astype(int)).sum() == len(fixed)
+            assert (after[fixed] == 0).all()
+            committed = np.where(before == 0)[0]
+            assert (s1["pre"]["tokens"][b, committed] == s0["pre"]["tokens"][b, committed]).all()
+    assert (tokens != mask_id).all()
+    if not gate:
+        assert (passes == S).all()                                   # dense horizon
+    elif m_req >= 1:
+        assert (passes >= min(m_req + 1, S)).all()                   # persistence needs repeats
+    assert 0.0 <= theory.step_ratio(passes, np.full_like(passes, S)) <= 1.0
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_gate_off_equals_unreachable_threshold(seed):
+    """Dense recovery: with the gate disabled the decoder is the original one, which is the
+    same as a threshold no confidence can reach (c <= 1 < 1.5)."""
+    V, P, G, blk, S = 19, 4, 16, 8, 8
+    model = _RandomModel(V, P + G, seed, scale=3.0)
+    prompt = np.random.default_rng(seed).integers(0, V - 1, (1, P))
+    t_off, p_off, _ = decode.block_decode(model, prompt, G, V - 1, blk, S, 0.65, 1, False)
+    t_hi, p_hi, _ = decode.block_decode(model, prompt, G, V - 1, blk, S, 1.5, 0, True)
+    t_end, p_end = decode.dense_endpoint(model, prompt, G, V - 1, blk, S)
+    assert (t_off == t_hi).all() and (p_off == p_hi).all() and (t_off == t_end).all()
+    assert (p_end == S).all()
+
+
+def test_accept_all_ends_each_block_in_one_pass():
+    V, P, G, blk, S = 17, 3, 32, 8, 8
+    model = _RandomModel(V, P + G, 7, scale=1.0)
+    prompt = np.zeros((2, P), dtype=np.int64)
+    _, passes, _ = decode.block_decode(model, prompt, G, V - 1, blk, S, 0.0, 0, True)
+    assert (passes == 1).all()
+
+
+def test_batch_rows_are_independent():
+    V, P, G, blk, S = 29, 4, 16, 8, 4
+    model = _RandomModel(V, P + G, 3, scale=4.0)
+    prompt = np.random.default_rng(9).integers(0, V - 1, (3, P))
+    t_all, p_all, _ = decode.block_decode(model, prompt, G, V - 1, blk, S, 0.4, 1, True)
+    for b in range(3):
+        t1, p1, _ = decode.block_decode(model, prompt[b:b + 1], G, V - 1, blk, S, 0.4, 1, True)
+        assert (t1[0] == t_all[b]).all() and (p1[0] == p_all[b]).all()
