@@ -1,0 +1,227 @@
+"""Throughput of the CORA-Diff denoising step on one MI355X.
+
+A step is one executed denoising pass over one batch: the dense bidirectional pass at
+the LLaDA-8B shape (32 layers, d 4096, 32 x 128 heads, SwiGLU 12288, vocab 126464), the
+LM head on the active block rows, and the fused vocab/gate kernel (top-1, confidence,
+persistence, transfer rule, residual gate, commit, termination).  Workload: batch 1,
+prompt 256 seeded random tokens + 256 generated positions, block 32, 32 steps per block,
+gate (0.65, 1), seeded N(0, 0.02) bf16 weights.
+
+Prints one JSON line.  value = denoising passes/s; also generated tokens/s, the
+roofline of the dominant kernel (gate/up SwiGLU GEMM, timed live with HIP events on the
+launching stream), the vocab/gate kernel's HBM roofline on bf16 logits [8, 512, 126464],
+a full gated block decode (passes per block, step ratio) and the CPU oracle baseline.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+B, P, G, BLK, S = 1, 256, 256, 32, 32
+DELTA_P, M_REQ = 0.65, 1
+
+
+def pass_flops(spec, M, rows):
+    """Algorithmic FLOPs of one dense pass: GEMMs + attention + LM head on `rows` rows."""
+    d, H, Hkv, hd, F, V = (spec.d_model, spec.n_heads, spec.n_kv_heads, spec.head_dim,
+                           spec.ffn_dim, spec.vocab)
+    L = M // B
+    per_layer = 2 * M * d * (H + 2 * Hkv) * hd + 2 * M * H * hd * d + 2 * M * d * 2 * F \
+        + 2 * M * F * d + 4 * B * H * L * L * hd
+    return spec.n_layers * per_layer + 2 * rows * d * V
+
+
+def gu_flops(spec, M):
+    return 2 * M * spec.d_model * 2 * spec.ffn_dim
+
+
+def cpu_baseline(spec, prompt, sample_layers=2, vocab_slice=16384):
+    """The oracle's dense pass on host cores, sampled: embedding + `sample_layers` of the
+    layers + the LM head over a `vocab_slice`-row slice of the vocabulary on the 32 block
+    rows, each part scaled to the full pass (layers x n_layers, LM head x V / slice)."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    import seeded_inputs as si
+    from oracle import forward as of
+
+    class _Slice:                      # LM head restricted to the first vocab_slice rows
+        def __init__(self, w, n):
+            self.final_norm, self._lm = w.final_norm, si.gen_rows(w.seed, si.TENSOR_LM_HEAD,
+                                                                  np.arange(n), spec.d_model)
+
+        def lm_head(self):
+            return self._lm
+
+    w = si.HostWeights(spec, 0, cache_layers=False)
+    tokens = np.concatenate([prompt, np.full((1, G), spec.mask_id, np.int32)], axis=1)[0]
+    L = tokens.shape[0]
+    cos, sin = of.rope_tables(L, spec.head_dim, spec.rope_theta, np.float64)
+    t0 = time.perf_counter()
+    h = np.asarray(w.embed_rows(tokens), dtype=np.float64)
+    t_embed = time.perf_counter() - t0
+    t_layers = 0.0
+    for i in range(sample_layers):
+        lw = w.layer(i)                              # input generation: not timed
+        t0 = time.perf_counter()
+        h = of.layer_forward(h, lw, spec, cos, sin, np.float64)
+        t_layers += time.perf_counter() - t0
+    sl = _Slice(w, vocab_slice)
+    t0 = time.perf_counter()
+    of.logits_from_hidden(sl, spec, h[P:P + BLK], np.float64)
+    t_lm = (time.perf_counter() - t0) * spec.vocab / vocab_slice
+    t_pass = t_embed + t_layers / sample_layers * spec.n_layers + t_lm
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    return {"value": 1.0 / t_pass, "unit": "passes/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"fp64 numpy oracle at L={L}: embedding + {sample_layers} of "
+                      f"{spec.n_layers} layers (scaled x{spec.n_layers / sample_layers:g}) + LM "
+                      f"head on {BLK} rows over {vocab_slice} of {spec.vocab} vocab rows (scaled); "
+                      f"{t_pass:.1f} s per full pass"}
+
+
+def vocab_gate_roofline(iters=20):
+    """HBM roofline of the vocab/gate kernel on bf16 logits [8, 512, 126464] (k = 1)."""
+    import numpy as np
+    import torch
+
+    import seeded_inputs as si
+    from paper_2608_11235_amd import DecodeState, Gate, Sched, vocab_gate, vocab_gate_workspace
+    w = si.vocab_gate_workload(seed=2)
+    Bv, R, V = w.logits_bits.shape
+    logits = torch.from_numpy(w.logits_bits.view(np.int16)).cuda()
+    L = w.state["tokens"].shape[1]
+    st = DecodeState.from_host(w.state, w.prompt_len, L - w.prompt_len, R, w.block_len)
+    ws = vocab_gate_workspace(Bv)
+    sc, gt = Sched(w.block_len, w.steps_per_block), Gate(DELTA_P, M_REQ, True)
+    for _ in range(3):
+        vocab_gate(logits, R, 0, V, w.mask_id, st, 1, sc, gt, ws)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(iters):
+        vocab_gate(logits, R, 0, V, w.mask_id, st, 1, sc, gt, ws)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / iters
+    nbytes = Bv * R * V * 2
+    ach = nbytes / (ms * 1e-3) / 1e9
+    return {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None, "us_per_launch": round(ms * 1e3, 2),
+            "workload": "bf16 logits [8, 512, 126464], k = 1"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-vocab", action="store_true")
+    ap.add_argument("--no-decode", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (batch rows "
+              "decode independently, so more GPUs shard rows with no collective)", file=sys.stderr)
+        sys.exit(2)
+    if args.warmup + args.steps > G:
+        sys.exit("warmup + steps must fit in one 256-pass decode")
+
+    import numpy as np
+    import torch
+
+    import seeded_inputs as si
+    from paper_2608_11235_amd import LLADA_8B, DecodeState, Gate, Model, Sched
+
+    spec = LLADA_8B
+    dev = torch.device("cuda:0")
+    prompt = si.prompt_tokens(1, B, P, spec.vocab, spec.mask_id)
+    t_create = time.perf_counter()
+    model = Model(spec, seed=0, max_batch=B, max_seq=P + G)
+    t_create = time.perf_counter() - t_create
+    sched, gate = Sched(BLK, S), Gate(DELTA_P, M_REQ, True)
+    host = si.initial_decode_state(prompt, G, spec.mask_id)
+    st = DecodeState.from_host(host, P, G, BLK, BLK, device=dev)
+
+    for _ in range(args.warmup):
+        model.denoise_step(st, sched, gate)
+    torch.cuda.synchronize()
+    unres0 = int(st.unresolved.sum())
+    model.set_timing(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        model.denoise_step(st, sched, gate)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    gu_ms, gu_launches = model.read_timing()
+    model.set_timing(False)
+    elapsed = t1 - t0
+    committed = unres0 - int(st.unresolved.sum())
+    passes_per_s = args.steps / elapsed
+    ms_per_step = elapsed * 1e3 / args.steps
+    M = B * (P + G)
+    fl_pass = pass_flops(spec, M, B * BLK)
+    gu_avg_ms = gu_ms / max(1, gu_launches)
+    gu_tflops = gu_flops(spec, M) / (gu_avg_ms * 1e-3) / 1e12
+
+    result = {
+        "metric": "denoising passes/s + gen tokens/s, LLaDA-8B shape gen256; MFMA util %",
+        "value": round(passes_per_s, 3),
+        "unit": "passes/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded random prompts, seeded N(0,0.02) weights)",
+        "config": {"workload": "llada8b-gen256", "batch": B, "prompt_len": P, "gen_len": G,
+                   "block_len": BLK, "steps_per_block": S, "gate": [DELTA_P, M_REQ]},
+        "gen_tokens_per_s": round(committed / elapsed, 3),
+        "pass_tflop": round(fl_pass / 1e12, 4),
+        "pass_mfma_frac": round(fl_pass / (ms_per_step * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "roofline": {"bound": "mfma", "achieved": round(gu_tflops, 1), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(gu_tflops / PEAK_BF16_TFLOPS, 4),
+                     "traffic": None, "kernel": "gate/up SwiGLU GEMM (M 512, N 24576, K 4096)",
+                     "us_per_launch": round(gu_avg_ms * 1e3, 2), "launches": gu_launches},
+        "model_create_s": round(t_create, 2),
+    }
+
+    if not args.no_decode:
+        pr = torch.from_numpy(prompt).to(dev)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        out, passes, total = model.block_decode(pr, G, sched, gate)
+        dt = time.perf_counter() - t0
+        dense = np.full_like(passes, S)
+        result["block_decode"] = {
+            "wall_s": round(dt, 3), "passes": int(passes.sum()), "dense_passes": int(dense.sum()),
+            "rho": round(float(passes.sum() / dense.sum()), 4),
+            "passes_per_s": round(int(total) / dt, 3), "gen_tokens_per_s": round(B * G / dt, 3),
+            "note": "random-init weights: top-1 confidence ~1e-3, so the gate never reaches 0.65",
+        }
+    model.close()
+    del model
+    torch.cuda.empty_cache()
+
+    if not args.no_vocab:
+        result["vocab_gate_roofline"] = vocab_gate_roofline()
+    if not args.no_cpu_baseline:
+        import seeded_inputs as si_
+        try:
+            result["cpu_baseline"] = cpu_baseline(si_.LLADA_8B, prompt)
+        except Exception as e:  # report, do not lose the GPU line
+            result["cpu_baseline"] = {"error": repr(e)}
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

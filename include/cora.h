@@ -1,0 +1,199 @@
+/* cora.h - C ABI of the MI355X (gfx950) CORA-Diff denoising-step library.
+ *
+ * One executed denoising step of blockwise masked-diffusion decoding (Section 3
+ * of the CORA-Diff paper, "Diffusion Decoding Setup" and "Confidence-Oriented
+ * Residual Acceptance"): a dense bidirectional Transformer pass over the whole
+ * prompt+generation canvas, per-position top-1 token and confidence (Eq. 1),
+ * the persistence counter (Eq. 2), the original low-confidence transfer rule,
+ * the residual confidence-and-persistence gate (Eq. 3), the commit of both
+ * sets (Eq. 4) and block termination once the active block holds no
+ * unresolved position (Fig. 2; "From acceptance to runtime").
+ *
+ * Conventions
+ *  - Every function returns cora_status (0 = CORA_OK, < 0 = error) and never
+ *    throws.  On error, cora_last_error() returns a thread-local message.
+ *  - "d_" pointers are device pointers, "h_" pointers are host pointers.  All
+ *    caller buffers stay owned by the caller.  The library owns the model
+ *    weights and a fixed workspace, both allocated in cora_model_create; no
+ *    other entry point allocates device memory.
+ *  - bf16 values cross the ABI as raw uint16_t bit patterns.
+ *  - Work is enqueued on the caller's HIP stream (`hip_stream`, a hipStream_t;
+ *    NULL = the default stream) in stream order.  Only cora_block_decode and
+ *    cora_model_copy_tensor wait on the host.
+ *  - Shapes are validated up front; unsupported shapes return
+ *    CORA_ERR_UNSUPPORTED, malformed arguments CORA_ERR_INVALID_ARG, HIP
+ *    failures CORA_ERR_HIP (with hipGetErrorString text in cora_last_error()).
+ */
+#ifndef CORA_H
+#define CORA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  CORA_OK = 0,
+  CORA_ERR_INVALID_ARG = -1,
+  CORA_ERR_UNSUPPORTED = -2,
+  CORA_ERR_OOM = -3,
+  CORA_ERR_HIP = -4,
+  CORA_ERR_STATE = -5
+} cora_status;
+
+#define CORA_MAX_BLOCK_LEN 256
+
+/* Backbone shape.  The paper keeps the backbone frozen and runs one dense pass
+ * per executed step (Section 3, first paragraph); the pass is a pre-norm
+ * bidirectional Transformer: RMSNorm, QKV projection (+ optional bias),
+ * rotate-half RoPE on q and k at absolute positions 0..L-1, non-causal
+ * softmax attention (grouped kv heads allowed), output projection, RMSNorm,
+ * SwiGLU MLP, final RMSNorm and an untied LM head scaled by logit_scale.
+ * Limits: head_dim in {64, 128}; n_heads % n_kv_heads == 0; d_model and
+ * n_heads*head_dim multiples of 64; vocab >= 2; 0 <= mask_id < vocab. */
+typedef struct {
+  int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, ffn_dim, vocab, mask_id;
+  int32_t qkv_bias; /* 0/1: bias on the q, k and v projections */
+  float rms_eps, rope_theta, logit_scale;
+  double init_std;  /* std of the seeded N(0, std) weights, e.g. 0.02 */
+} cora_model_cfg;
+
+/* Blockwise schedule: the generation region is split into blocks of
+ * block_len positions decoded left to right, each with a fixed horizon of
+ * steps_per_block executed steps (Section 3, "Diffusion Decoding Setup").
+ * The transfer rule fixes k_s = floor(block_len / S) + [s < block_len mod S]
+ * positions at block step s (a linear split of the block's masked positions).
+ * 1 <= steps_per_block <= block_len <= CORA_MAX_BLOCK_LEN. */
+typedef struct {
+  int32_t block_len, steps_per_block;
+} cora_sched_cfg;
+
+/* Residual gate of Eq. (3): accept i iff c_i >= delta_p and m_i >= m_req,
+ * both inclusive, on unresolved active-block positions the transfer rule did
+ * not fix.  gate_enabled = 0 gives the original dense decoder (no position
+ * accepted).  persist_scope: 0 = BLOCK (counters reset when a block becomes
+ * active; the only scope implemented, others return CORA_ERR_UNSUPPORTED). */
+typedef struct {
+  float delta_p;
+  int32_t m_req, gate_enabled, persist_scope;
+} cora_gate_cfg;
+
+/* Decode state of a batch of independent rows, all device pointers, updated
+ * in place.  B rows, canvas length L = prompt_len + gen_len, gen_len a
+ * multiple of block_len, n_blocks = gen_len / block_len.
+ *   tokens     int32 [B, L]   canvas x; mask_id where masked
+ *   unresolved uint8 [B, L]   1 iff the position is in U
+ *   prev_top1  int32 [B, L]   top-1 of the previous executed step, -1 = none
+ *   persist    int32 [B, L]   persistence counter m (Eq. 2)
+ *   block_idx  int32 [B]      active block; n_blocks once the row is finished
+ *   step_idx   int32 [B]      executed steps so far in the active block
+ *   top1, conf int32/float [B, n_rows]  Eq. (1) outputs of the scored rows
+ *   decision   uint8 [B, block_len]     0 none, 1 fixed by the transfer
+ *                                       rule, 2 accepted by the gate
+ *   done       int32 [B]      1 iff the active block was resolved by this step
+ *                             (or the row was already finished)
+ *   passes     int32 [B, n_blocks] or NULL: executed passes per block,
+ *                             incremented for every row still decoding */
+typedef struct {
+  int32_t *tokens;
+  uint8_t *unresolved;
+  int32_t *prev_top1;
+  int32_t *persist;
+  int32_t *block_idx;
+  int32_t *step_idx;
+  int32_t *top1;
+  float *conf;
+  uint8_t *decision;
+  int32_t *done;
+  int32_t *passes;
+  int32_t B, prompt_len, gen_len;
+} cora_state;
+
+typedef struct cora_model cora_model;
+
+/* Allocate weights and workspace for batches of up to max_batch rows of up to
+ * max_seq positions, and fill every weight with the counter-based generator:
+ * element e (row-major [out, in]) of tensor t is
+ *   key = mix(seed); ctr = (t << 40) | e;
+ *   h1 = mix(key + (2 ctr + 1) G), h2 = mix(key + (2 ctr + 2) G),
+ *   u1 = ((h1 >> 11) + 1) 2^-53, u2 = (h2 >> 11) 2^-53,
+ *   w  = bf16_rne(float_rne(init_std * sqrt(-2 ln u1) cos(2 pi u2)))
+ * with mix the SplitMix64 finaliser and G = 0x9E3779B97F4A7C15.  Tensor ids:
+ * 1 embedding [V, d], 2 LM head [V, d], and 100 + 16 l + j for layer l with
+ * j = 0 wq, 1 wk, 2 wv, 3 wo, 4 wg, 5 wu, 6 wd, 7 bq, 8 bk, 9 bv.  Norm
+ * weights are 1.  Synchronous.  *out is set only on success. */
+cora_status cora_model_create(const cora_model_cfg *cfg, uint64_t seed, int32_t max_batch,
+                              int32_t max_seq, void *hip_stream, cora_model **out);
+cora_status cora_model_destroy(cora_model *model);
+
+/* Dense forward pass over tokens [B, L] (int32, device) and the LM head on
+ * canvas rows [row_begin, row_begin + n_rows) of every batch row: writes
+ * bf16 logits [B, n_rows, V] (device, caller-allocated).  Parity hook. */
+cora_status cora_forward_logits(cora_model *model, const int32_t *d_tokens, int32_t B, int32_t L,
+                                int32_t row_begin, int32_t n_rows, uint16_t *d_logits,
+                                void *hip_stream);
+
+/* One executed denoising step on every row of `state` that is still decoding:
+ * dense pass, LM head on the active block rows of each batch row, then the
+ * vocab/gate kernel (Eq. 1, Eq. 2, transfer rule, Eq. 3, Eq. 4, termination;
+ * see cora_vocab_gate).  top1/conf are [B, block_len].  Asynchronous. */
+cora_status cora_denoise_step(cora_model *model, cora_state *state, const cora_sched_cfg *sched,
+                              const cora_gate_cfg *gate, void *hip_stream);
+
+/* The vocab/gate kernel alone on caller logits.  d_logits: bf16 [B, n_rows, V];
+ * row r of batch row b scores canvas position row_begin + r, or, when
+ * row_begin < 0, position lo_b + r where lo_b is the first position of b's
+ * active block.  For every row: top-1 token (lowest id among equal maxima,
+ * mask_id never predicted) and confidence c = 1 / sum_v exp(l_v - l_max)
+ * (fp32).  Then, per batch row still decoding, on its active block: counters
+ * reset at block step 0, persistence update on unresolved positions, the
+ * k highest-confidence unresolved positions (ties: lower position) fixed
+ * (k = k_transfer if >= 0, else the schedule's k_s), the gate on the rest,
+ * commit of both sets, and the block/step advance once the block is empty.
+ * A fixed row_begin must cover the whole generation region.
+ * d_workspace: at least cora_vocab_gate_workspace_bytes(B) bytes of device
+ * memory, zero before the first call; every call leaves it zero again.
+ * Calls sharing one workspace must not overlap.  Asynchronous. */
+size_t cora_vocab_gate_workspace_bytes(int32_t B);
+cora_status cora_vocab_gate(const uint16_t *d_logits, int32_t n_rows, int32_t row_begin,
+                            int32_t V, int32_t mask_id, cora_state *state, int32_t k_transfer,
+                            const cora_sched_cfg *sched, const cora_gate_cfg *gate,
+                            void *d_workspace, size_t workspace_bytes, void *hip_stream);
+
+/* Gated block decode of B prompts (d_prompt int32 [B, prompt_len], device):
+ * the canvas starts as prompt + gen_len masks, rows decode independently and
+ * each block ends once it holds no unresolved position, skipping its
+ * remaining passes.  Writes the final canvas to d_out_tokens int32 [B, L]
+ * (device) and the executed passes per block to h_passes int32
+ * [B, gen_len / block_len] (host).  If h_total_passes is not NULL it receives
+ * the number of dense passes launched (the batch runs while any row decodes).
+ * Synchronous on return. */
+cora_status cora_block_decode(cora_model *model, const int32_t *d_prompt, int32_t B,
+                              int32_t prompt_len, int32_t gen_len, const cora_sched_cfg *sched,
+                              const cora_gate_cfg *gate, int32_t *d_out_tokens, int32_t *h_passes,
+                              int32_t *h_total_passes, void *hip_stream);
+
+/* Copy weight tensor `tensor_id` (ids as in cora_model_create) to host memory
+ * in its logical row-major [out, in] layout as bf16 bits (biases too).
+ * `bytes` must equal the tensor's size.  Synchronous. */
+cora_status cora_model_copy_tensor(cora_model *model, int32_t tensor_id, void *h_dst, size_t bytes);
+
+/* Kernel timing: when enabled, the library brackets every launch of the
+ * gate/up SwiGLU GEMM with HIP events on the launching stream.  Reading
+ * returns the summed event time (ms) and the number of launches since the
+ * last reset, waiting for the recorded events. */
+cora_status cora_model_set_timing(cora_model *model, int32_t enable);
+cora_status cora_model_read_timing(cora_model *model, double *total_ms, int64_t *launches);
+
+/* Device bytes the model holds (weights + workspace). */
+cora_status cora_model_device_bytes(cora_model *model, size_t *weight_bytes, size_t *workspace_bytes);
+
+const char *cora_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CORA_H */

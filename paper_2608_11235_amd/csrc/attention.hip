@@ -1,0 +1,155 @@
+// Bidirectional (non-causal) attention for gfx950, online softmax in fp32.
+//
+// Inputs: q [B, H, Ls, hd], k [B, Hkv, Ls, hd] (RoPE applied), vt [B, Hkv, hd, Ls]
+// (v transposed), rows >= L zero.  Output: o [B * L, H * hd] bf16.
+// One workgroup = 64 queries of one head (4 wavefronts x 16 queries); key tiles of 64
+// are staged in LDS.  Everything is computed transposed with
+// v_mfma_f32_16x16x32_bf16 so that a query's softmax statistics never leave its lanes:
+//   S^T = K Q^T   (A = K tile from LDS, B = Q^T held in registers)
+//   O^T = V^T P^T (A = V^T tile from LDS, B = P^T straight from the S^T registers)
+// In S^T a lane holds keys 16kb + 4(lane/16) + i of query lane%16; feeding those
+// registers as P^T fixes the key order of one 32-key MFMA step, and the V^T fragment
+// is read from LDS in that same order.
+#include "common.hpp"
+#include "internal.hpp"
+
+namespace cora {
+
+template <int HD>
+__global__ __launch_bounds__(256) void k_attention(const uint16_t* __restrict__ q,
+                                                   const uint16_t* __restrict__ k,
+                                                   const uint16_t* __restrict__ vt,
+                                                   uint16_t* __restrict__ out, int L, int Ls,
+                                                   int H, int Hkv, float scale_log2) {
+  constexpr int KT = 64;          // keys per tile
+  constexpr int LDKS = HD + 8;    // padded LDS rows
+  constexpr int LDVS = KT + 8;
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[KT * LDKS];
+  __shared__ __attribute__((aligned(16))) uint16_t Vs[HD * LDVS];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int bh = blockIdx.y, b = bh / H, h = bh % H, kvh = h / (H / Hkv);
+  const int q0 = blockIdx.x * 64 + wave * 16;
+  const int g = lane >> 4, r16 = lane & 15;
+
+  const uint16_t* qh = q + ((int64_t)(b * H + h) * Ls) * HD;
+  const uint16_t* kh = k + ((int64_t)(b * Hkv + kvh) * Ls) * HD;
+  const uint16_t* vh = vt + ((int64_t)(b * Hkv + kvh) * HD) * Ls;
+
+  bf16x8_t qf[HD / 32];
+#pragma unroll
+  for (int kk = 0; kk < HD / 32; ++kk)
+    qf[kk] = as_bf16x8(*reinterpret_cast<const u32x4_t*>(qh + (int64_t)(q0 + r16) * HD + kk * 32 + g * 8));
+
+  f32x4_t o[HD / 16];
+#pragma unroll
+  for (int d = 0; d < HD / 16; ++d) o[d] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY, l_part = 0.f;
+
+  const int n_tiles = (L + KT - 1) / KT;
+  for (int kt = 0; kt < n_tiles; ++kt) {
+    const int key0 = kt * KT;
+    // stage K [64][HD] and V^T [HD][64]
+    for (int c = tid; c < KT * HD / 8; c += 256) {
+      const int r = c / (HD / 8), cc = (c % (HD / 8)) * 8;
+      *reinterpret_cast<u32x4_t*>(&Ks[r * LDKS + cc]) =
+          *reinterpret_cast<const u32x4_t*>(kh + (int64_t)(key0 + r) * HD + cc);
+    }
+    for (int c = tid; c < HD * KT / 8; c += 256) {
+      const int r = c / (KT / 8), cc = (c % (KT / 8)) * 8;
+      *reinterpret_cast<u32x4_t*>(&Vs[r * LDVS + cc]) =
+          *reinterpret_cast<const u32x4_t*>(vh + (int64_t)r * Ls + key0 + cc);
+    }
+    __syncthreads();
+
+    f32x4_t st[4];
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      st[kb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < HD / 32; ++kk) {
+        const bf16x8_t a = as_bf16x8(
+            *reinterpret_cast<const u32x4_t*>(&Ks[(kb * 16 + r16) * LDKS + kk * 32 + g * 8]));
+        st[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[kk], st[kb], 0, 0, 0);
+      }
+    }
+    float tmax = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int key = key0 + kb * 16 + g * 4 + i;
+        const float v = key < L ? st[kb][i] * scale_log2 : -INFINITY;
+        st[kb][i] = v;
+        tmax = fmaxf(tmax, v);
+      }
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+    const float m_new = fmaxf(m_run, tmax);
+    const float alpha = exp2f(m_run - m_new);
+    m_run = m_new;
+    l_part *= alpha;
+#pragma unroll
+    for (int d = 0; d < HD / 16; ++d) o[d] *= alpha;
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float p = exp2f(st[kb][i] - m_new);
+        st[kb][i] = p;
+        l_part += p;
+      }
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      u32x4_t pb;
+      pb.x = pack_bf16x2(st[2 * ks][0], st[2 * ks][1]);
+      pb.y = pack_bf16x2(st[2 * ks][2], st[2 * ks][3]);
+      pb.z = pack_bf16x2(st[2 * ks + 1][0], st[2 * ks + 1][1]);
+      pb.w = pack_bf16x2(st[2 * ks + 1][2], st[2 * ks + 1][3]);
+      const bf16x8_t bfrag = as_bf16x8(pb);
+#pragma unroll
+      for (int d = 0; d < HD / 16; ++d) {
+        const uint16_t* vrow = &Vs[(d * 16 + r16) * LDVS + ks * 32 + g * 4];
+        const u32x2_t lo = *reinterpret_cast<const u32x2_t*>(vrow);
+        const u32x2_t hi = *reinterpret_cast<const u32x2_t*>(vrow + 16);
+        const u32x4_t av = u32x4_t{lo.x, lo.y, hi.x, hi.y};
+        o[d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(av), bfrag, o[d], 0, 0, 0);
+      }
+    }
+    __syncthreads();
+  }
+
+  float l = l_part;
+  l += __shfl_xor(l, 16, 64);
+  l += __shfl_xor(l, 32, 64);
+  const float inv = 1.0f / l;
+  const int qi = q0 + r16;
+  if (qi < L) {
+    uint16_t* dst = out + ((int64_t)b * L + qi) * ((int64_t)H * HD) + h * HD;
+#pragma unroll
+    for (int d = 0; d < HD / 16; ++d) {
+      u32x2_t p;
+      p.x = pack_bf16x2(o[d][0] * inv, o[d][1] * inv);
+      p.y = pack_bf16x2(o[d][2] * inv, o[d][3] * inv);
+      *reinterpret_cast<u32x2_t*>(dst + d * 16 + g * 4) = p;
+    }
+  }
+}
+
+hipError_t launch_attention(const uint16_t* q, const uint16_t* k, const uint16_t* vt,
+                            uint16_t* out, int B, int L, int Ls, int H, int Hkv, int hd,
+                            hipStream_t s) {
+  const float scale_log2 = 1.4426950408889634f / sqrtf((float)hd);
+  const dim3 grid(Ls / 64, B * H);
+  if (hd == 128)
+    hipLaunchKernelGGL(k_attention<128>, grid, dim3(256), 0, s, q, k, vt, out, L, Ls, H, Hkv,
+                       scale_log2);
+  else if (hd == 64)
+    hipLaunchKernelGGL(k_attention<64>, grid, dim3(256), 0, s, q, k, vt, out, L, Ls, H, Hkv,
+                       scale_log2);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+}  // namespace cora

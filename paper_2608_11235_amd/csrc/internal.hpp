@@ -1,0 +1,79 @@
+// Host-side launch wrappers shared by the runtime (not part of the C ABI).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace cora {
+
+// ---- weight init (K10) ------------------------------------------------------------------
+// Physical row of logical row r: 0 identity (+row_offset), 1 gate half and 2 up half of
+// the 32-row interleaved gate/up matrix.
+enum RowMap { ROW_IDENTITY = 0, ROW_GATE = 1, ROW_UP = 2 };
+hipError_t launch_init_bf16(uint16_t* dst, uint64_t seed, uint64_t tensor_id, int64_t rows,
+                            int64_t cols, int64_t ld, int row_map, int64_t row_offset, double std_dev,
+                            hipStream_t s);
+hipError_t launch_init_f32(float* dst, uint64_t seed, uint64_t tensor_id, int64_t n, double std_dev,
+                           hipStream_t s);
+hipError_t launch_fill_f32(float* dst, float v, int64_t n, hipStream_t s);
+
+// ---- elementwise ------------------------------------------------------------------------
+hipError_t launch_embed(const int32_t* tokens, const uint16_t* E, float* h, int M, int d, int V,
+                        hipStream_t s);
+// out[j] = rmsnorm(h[src(j)]) with src(j) = j (mode 0), or for j = b * n_rows + r:
+// b * L + row_begin + r (mode 1), b * L + lo_b + r with lo_b the active block start (mode 2).
+struct RowSel {
+  int mode, L, n_rows, row_begin, prompt_len, block_len, n_blocks;
+  const int32_t* block_idx;
+};
+hipError_t launch_rmsnorm(const float* h, const float* w, uint16_t* out, int rows, int d,
+                          float eps, RowSel sel, hipStream_t s);
+hipError_t launch_rope_split(const uint16_t* qkv, uint16_t* q, uint16_t* k, uint16_t* vt,
+                             const float* cos_t, const float* sin_t, int B, int L, int Ls, int H,
+                             int Hkv, int hd, hipStream_t s);
+hipError_t launch_state_init(const int32_t* prompt, int B, int P, int G, int mask_id,
+                             int32_t* tokens, uint8_t* unresolved, int32_t* prev, int32_t* persist,
+                             int32_t* block_idx, int32_t* step_idx, int32_t* passes, int n_blocks,
+                             hipStream_t s);
+
+// ---- GEMM: C[M, N] = A[M, K] . W[N, K]^T, bf16 in, fp32 accumulate ---------------------
+enum GemmEpi { EPI_BF16 = 0, EPI_ADD_F32 = 1, EPI_SWIGLU = 2 };
+struct GemmArgs {
+  const uint16_t* A; int64_t lda;
+  const uint16_t* W; int64_t ldw;
+  int M, N, K;
+  void* C; int64_t ldc;
+  const float* bias;   // EPI_BF16: per-column bias (or null)
+  float scale;         // EPI_BF16: multiplier after the bias
+  int splits;          // set by launch_gemm from the plan
+  float* ws;           // split-K partials (GemmPlan::ws_floats floats)
+  int32_t* counters;   // split-K tickets, one per tile, zero on entry and exit
+};
+struct GemmPlan {
+  int cfg, tiles, splits;
+  size_t ws_floats;
+};
+// Tile configuration and K split for one GEMM shape.  Split-K workspace never exceeds
+// gemm_ws_floats_bound(num_cus) floats and num_cus tickets.
+GemmPlan gemm_plan(int epi, int M, int N, int K, int num_cus);
+inline size_t gemm_ws_floats_bound(int num_cus) { return (size_t)2 * num_cus * 256 * 128; }
+hipError_t launch_gemm(int epi, const GemmArgs& a, const GemmPlan& p, hipStream_t s);
+
+// ---- attention ---------------------------------------------------------------------------
+hipError_t launch_attention(const uint16_t* q, const uint16_t* k, const uint16_t* vt,
+                            uint16_t* out, int B, int L, int Ls, int H, int Hkv, int hd,
+                            hipStream_t s);
+
+// ---- vocab / gate (K9) -------------------------------------------------------------------
+struct VocabGateArgs {
+  const uint16_t* logits; int n_rows; int row_begin; int V; int mask_id;
+  int32_t* tokens; uint8_t* unresolved; int32_t* prev_top1; int32_t* persist;
+  int32_t* block_idx; int32_t* step_idx; int32_t* top1; float* conf; uint8_t* decision;
+  int32_t* done; int32_t* passes;
+  int B, L, prompt_len, block_len, steps_per_block, n_blocks;
+  int k_transfer;  // >= 0 fixed k, < 0: schedule
+  float delta_p; int m_req; int gate_enabled;
+  int32_t* tickets;  // [B], zero on entry and exit
+};
+hipError_t launch_vocab_gate(const VocabGateArgs& a, hipStream_t s);
+
+}  // namespace cora

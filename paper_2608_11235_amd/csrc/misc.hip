@@ -1,0 +1,255 @@
+// Weight init (counter-based generator), embedding gather, RMSNorm, RoPE + head
+// split, and decode-state init.
+#include "common.hpp"
+#include "internal.hpp"
+
+namespace cora {
+
+// ---- counter-based N(0, std) generator ---------------------------------------------------
+// SplitMix64 finaliser; the stream started at key = mix(seed) yields outputs 2c+1 and 2c+2
+// for counter c = (tensor_id << 40) | element; Box-Muller in fp64; round to fp32 then bf16.
+__device__ __forceinline__ uint64_t mix64(uint64_t z) {
+  z ^= z >> 30;
+  z *= 0xBF58476D1CE4E5B9ULL;
+  z ^= z >> 27;
+  z *= 0x94D049BB133111EBULL;
+  z ^= z >> 31;
+  return z;
+}
+
+__device__ __forceinline__ float normal_from_counter(uint64_t key, uint64_t ctr, double std_dev) {
+  const uint64_t G = 0x9E3779B97F4A7C15ULL;
+  const uint64_t h1 = mix64(key + (2 * ctr + 1) * G);
+  const uint64_t h2 = mix64(key + (2 * ctr + 2) * G);
+  const double u1 = (double)((h1 >> 11) + 1) * 0x1.0p-53;
+  const double u2 = (double)(h2 >> 11) * 0x1.0p-53;
+  const double n = sqrt(-2.0 * log(u1)) * cos(6.283185307179586476925286766559 * u2);
+  return (float)(std_dev * n);
+}
+
+__global__ void k_init_bf16(uint16_t* __restrict__ dst, uint64_t key, uint64_t base, int64_t rows,
+                            int64_t cols, int64_t ld, int row_map, int64_t row_offset,
+                            double std_dev) {
+  for (int64_t r = blockIdx.x; r < rows; r += gridDim.x) {
+    int64_t pr;
+    if (row_map == ROW_GATE) pr = (r >> 5) * 64 + (r & 31);
+    else if (row_map == ROW_UP) pr = (r >> 5) * 64 + 32 + (r & 31);
+    else pr = row_offset + r;
+    uint16_t* out = dst + pr * ld;
+    for (int64_t c = threadIdx.x; c < cols; c += blockDim.x) {
+      const uint64_t ctr = base | (uint64_t)(r * cols + c);
+      out[c] = (uint16_t)f32_to_bf16_bits(normal_from_counter(key, ctr, std_dev));
+    }
+  }
+}
+
+// bias vectors: drawn like any tensor, rounded to bf16, stored as fp32
+__global__ void k_init_f32(float* __restrict__ dst, uint64_t key, uint64_t base, int64_t n,
+                           double std_dev) {
+  for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < n;
+       e += (int64_t)gridDim.x * blockDim.x) {
+    const float v = normal_from_counter(key, base | (uint64_t)e, std_dev);
+    dst[e] = bf16_bits_to_f32(f32_to_bf16_bits(v));
+  }
+}
+
+__global__ void k_fill_f32(float* dst, float v, int64_t n) {
+  for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < n;
+       e += (int64_t)gridDim.x * blockDim.x)
+    dst[e] = v;
+}
+
+static uint64_t host_mix64(uint64_t z) {
+  z ^= z >> 30;
+  z *= 0xBF58476D1CE4E5B9ULL;
+  z ^= z >> 27;
+  z *= 0x94D049BB133111EBULL;
+  z ^= z >> 31;
+  return z;
+}
+
+hipError_t launch_init_bf16(uint16_t* dst, uint64_t seed, uint64_t tensor_id, int64_t rows,
+                            int64_t cols, int64_t ld, int row_map, int64_t row_offset, double std_dev,
+                            hipStream_t s) {
+  const int grid = (int)(rows < 16384 ? rows : 16384);
+  hipLaunchKernelGGL(k_init_bf16, dim3(grid), dim3(256), 0, s, dst, host_mix64(seed),
+                     tensor_id << 40, rows, cols, ld, row_map, row_offset, std_dev);
+  return hipGetLastError();
+}
+
+hipError_t launch_init_f32(float* dst, uint64_t seed, uint64_t tensor_id, int64_t n,
+                           double std_dev, hipStream_t s) {
+  const int grid = (int)((n + 255) / 256 < 4096 ? (n + 255) / 256 : 4096);
+  hipLaunchKernelGGL(k_init_f32, dim3(grid), dim3(256), 0, s, dst, host_mix64(seed),
+                     tensor_id << 40, n, std_dev);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_f32(float* dst, float v, int64_t n, hipStream_t s) {
+  const int grid = (int)((n + 255) / 256 < 4096 ? (n + 255) / 256 : 4096);
+  hipLaunchKernelGGL(k_fill_f32, dim3(grid), dim3(256), 0, s, dst, v, n);
+  return hipGetLastError();
+}
+
+// ---- embedding: h[m, :] = E[tokens[m], :] (fp32 residual stream) ------------------------
+__global__ void k_embed(const int32_t* __restrict__ tokens, const uint16_t* __restrict__ E,
+                        float* __restrict__ h, int d, int V) {
+  const int m = blockIdx.x;
+  const int tok = min(max(tokens[m], 0), V - 1);  // out-of-range ids never read outside E
+  const uint16_t* src = E + (int64_t)tok * d;
+  float* dst = h + (int64_t)m * d;
+  for (int c = threadIdx.x * 8; c < d; c += blockDim.x * 8) {
+    const u32x4_t v = *reinterpret_cast<const u32x4_t*>(src + c);
+    float4 lo, hi;
+    lo.x = bf16_bits_to_f32(v.x & 0xffff); lo.y = bf16_bits_to_f32(v.x >> 16);
+    lo.z = bf16_bits_to_f32(v.y & 0xffff); lo.w = bf16_bits_to_f32(v.y >> 16);
+    hi.x = bf16_bits_to_f32(v.z & 0xffff); hi.y = bf16_bits_to_f32(v.z >> 16);
+    hi.z = bf16_bits_to_f32(v.w & 0xffff); hi.w = bf16_bits_to_f32(v.w >> 16);
+    *reinterpret_cast<float4*>(dst + c) = lo;
+    *reinterpret_cast<float4*>(dst + c + 4) = hi;
+  }
+}
+
+hipError_t launch_embed(const int32_t* tokens, const uint16_t* E, float* h, int M, int d, int V,
+                        hipStream_t s) {
+  if (M == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_embed, dim3(M), dim3(256), 0, s, tokens, E, h, d, V);
+  return hipGetLastError();
+}
+
+// ---- RMSNorm: fp32 rows in, bf16 rows out ------------------------------------------------
+__global__ __launch_bounds__(256) void k_rmsnorm(const float* __restrict__ h,
+                                                 const float* __restrict__ w,
+                                                 uint16_t* __restrict__ out, int d, float eps,
+                                                 RowSel sel) {
+  const int j = blockIdx.x;
+  int64_t src = j;
+  if (sel.mode != 0) {
+    const int b = j / sel.n_rows, r = j % sel.n_rows;
+    int base = sel.row_begin;
+    if (sel.mode == 2) {
+      int blk = sel.block_idx[b];
+      blk = max(0, min(blk, sel.n_blocks - 1));
+      base = sel.prompt_len + blk * sel.block_len;
+    }
+    src = (int64_t)b * sel.L + base + r;
+  }
+  const float* x = h + src * d;
+  float ss = 0.f;
+  for (int c = threadIdx.x * 4; c < d; c += 256 * 4) {
+    const float4 v = *reinterpret_cast<const float4*>(x + c);
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  }
+  ss = warp_sum(ss);
+  __shared__ float part[4];
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  const float tot = part[0] + part[1] + part[2] + part[3];
+  const float inv = 1.0f / sqrtf(tot / (float)d + eps);
+  uint16_t* o = out + (int64_t)j * d;
+  for (int c = threadIdx.x * 4; c < d; c += 256 * 4) {
+    const float4 v = *reinterpret_cast<const float4*>(x + c);
+    const float4 g = *reinterpret_cast<const float4*>(w + c);
+    u32x2_t p;
+    p.x = pack_bf16x2(v.x * inv * g.x, v.y * inv * g.y);
+    p.y = pack_bf16x2(v.z * inv * g.z, v.w * inv * g.w);
+    *reinterpret_cast<u32x2_t*>(o + c) = p;
+  }
+}
+
+hipError_t launch_rmsnorm(const float* h, const float* w, uint16_t* out, int rows, int d,
+                          float eps, RowSel sel, hipStream_t s) {
+  if (rows == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_rmsnorm, dim3(rows), dim3(256), 0, s, h, w, out, d, eps, sel);
+  return hipGetLastError();
+}
+
+// ---- RoPE (rotate-half) on q and k, head-major split, v transposed ----------------------
+// qkv [B*L, (H + 2 Hkv) * hd] -> q [B, H, Ls, hd], k [B, Hkv, Ls, hd], vt [B, Hkv, hd, Ls];
+// positions L..Ls-1 are written as zeros.  One block = 64 positions of one head.
+__global__ __launch_bounds__(256) void k_rope_split(const uint16_t* __restrict__ qkv,
+                                                    uint16_t* __restrict__ q,
+                                                    uint16_t* __restrict__ k,
+                                                    uint16_t* __restrict__ vt,
+                                                    const float* __restrict__ cos_t,
+                                                    const float* __restrict__ sin_t, int L,
+                                                    int Ls, int H, int Hkv, int hd) {
+  const int p0 = blockIdx.x * 64, b = blockIdx.y, hh = blockIdx.z;
+  const int ldq = (H + 2 * Hkv) * hd;
+  const int half = hd / 2;
+  if (hh < H + Hkv) {
+    uint16_t* dst;
+    if (hh < H) dst = q + ((int64_t)(b * H + hh) * Ls) * hd;
+    else dst = k + ((int64_t)(b * Hkv + (hh - H)) * Ls) * hd;
+    for (int e = threadIdx.x; e < 64 * half; e += 256) {
+      const int p = e / half, j = e % half, pos = p0 + p;
+      float o1 = 0.f, o2 = 0.f;
+      if (pos < L) {
+        const uint16_t* src = qkv + ((int64_t)b * L + pos) * ldq + hh * hd;
+        const float x1 = bf16_bits_to_f32(src[j]), x2 = bf16_bits_to_f32(src[j + half]);
+        const float c = cos_t[pos * half + j], sn = sin_t[pos * half + j];
+        o1 = x1 * c - x2 * sn;
+        o2 = x2 * c + x1 * sn;
+      }
+      dst[(int64_t)pos * hd + j] = (uint16_t)f32_to_bf16_bits(o1);
+      dst[(int64_t)pos * hd + j + half] = (uint16_t)f32_to_bf16_bits(o2);
+    }
+  } else {
+    __shared__ uint16_t tile[64][128 + 2];
+    const int kvh = hh - H - Hkv;
+    for (int e = threadIdx.x; e < 64 * hd; e += 256) {
+      const int p = e / hd, c = e % hd, pos = p0 + p;
+      tile[p][c] = pos < L ? qkv[((int64_t)b * L + pos) * ldq + hh * hd + c] : (uint16_t)0;
+    }
+    __syncthreads();
+    uint16_t* dst = vt + ((int64_t)(b * Hkv + kvh) * hd) * Ls;
+    for (int e = threadIdx.x; e < 64 * hd; e += 256) {
+      const int c = e / 64, p = e % 64;
+      dst[(int64_t)c * Ls + p0 + p] = tile[p][c];
+    }
+  }
+}
+
+hipError_t launch_rope_split(const uint16_t* qkv, uint16_t* q, uint16_t* k, uint16_t* vt,
+                             const float* cos_t, const float* sin_t, int B, int L, int Ls, int H,
+                             int Hkv, int hd, hipStream_t s) {
+  hipLaunchKernelGGL(k_rope_split, dim3(Ls / 64, B, H + 2 * Hkv), dim3(256), 0, s, qkv, q, k, vt,
+                     cos_t, sin_t, L, Ls, H, Hkv, hd);
+  return hipGetLastError();
+}
+
+// ---- decode state: canvas = prompt ++ masks --------------------------------------------
+__global__ void k_state_init(const int32_t* __restrict__ prompt, int B, int P, int G, int mask_id,
+                             int32_t* tokens, uint8_t* unresolved, int32_t* prev, int32_t* persist,
+                             int32_t* block_idx, int32_t* step_idx, int32_t* passes,
+                             int n_blocks) {
+  const int L = P + G;
+  const int64_t n = (int64_t)B * L;
+  for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < n;
+       e += (int64_t)gridDim.x * blockDim.x) {
+    const int b = (int)(e / L), i = (int)(e % L);
+    tokens[e] = i < P ? prompt[(int64_t)b * P + i] : mask_id;
+    unresolved[e] = i < P ? 0 : 1;
+    prev[e] = -1;
+    persist[e] = 0;
+    if (i == 0) {
+      block_idx[b] = 0;
+      step_idx[b] = 0;
+      if (passes)
+        for (int j = 0; j < n_blocks; ++j) passes[(int64_t)b * n_blocks + j] = 0;
+    }
+  }
+}
+
+hipError_t launch_state_init(const int32_t* prompt, int B, int P, int G, int mask_id,
+                             int32_t* tokens, uint8_t* unresolved, int32_t* prev, int32_t* persist,
+                             int32_t* block_idx, int32_t* step_idx, int32_t* passes, int n_blocks,
+                             hipStream_t s) {
+  const int64_t n = (int64_t)B * (P + G);
+  const int grid = (int)((n + 255) / 256 < 1024 ? (n + 255) / 256 : 1024);
+  hipLaunchKernelGGL(k_state_init, dim3(grid), dim3(256), 0, s, prompt, B, P, G, mask_id, tokens,
+                     unresolved, prev, persist, block_idx, step_idx, passes, n_blocks);
+  return hipGetLastError();
+}
+
+}  // namespace cora

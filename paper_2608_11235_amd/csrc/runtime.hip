@@ -1,0 +1,597 @@
+// Host runtime behind the C ABI: model and workspace ownership, the launch
+// sequence of one dense pass, the denoising step, and the gated block decode loop.
+#include <math.h>
+#include <string.h>
+
+#include <string>
+#include <vector>
+
+#include "common.hpp"
+#include "internal.hpp"
+
+using namespace cora;
+
+namespace {
+
+thread_local std::string g_err;
+
+cora_status fail(cora_status st, const std::string& msg) {
+  g_err = msg;
+  return st;
+}
+
+#define HIP_TRY(expr)                                                                   \
+  do {                                                                                  \
+    hipError_t e_ = (expr);                                                             \
+    if (e_ != hipSuccess)                                                               \
+      return fail(CORA_ERR_HIP, std::string(#expr) + ": " + hipGetErrorString(e_));    \
+  } while (0)
+
+constexpr size_t ALIGN = 256;
+inline size_t align_up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
+inline int round_up(int x, int m) { return (x + m - 1) / m * m; }
+
+// bump allocator over one device allocation
+struct Arena {
+  char* base = nullptr;
+  size_t used = 0, cap = 0;
+  template <class T>
+  T* take(size_t n) {
+    T* p = reinterpret_cast<T*>(base + used);
+    used += align_up(n * sizeof(T));
+    return p;
+  }
+};
+
+}  // namespace
+
+struct cora_model {
+  cora_model_cfg cfg{};
+  int max_batch = 0, max_seq = 0, max_seq_pad = 0, max_rows = 0;
+  int hq = 0, hkv = 0, qkv_n = 0, f_pad = 0;
+  void* weight_mem = nullptr;
+  void* ws_mem = nullptr;
+  size_t weight_bytes = 0, ws_bytes = 0;
+
+  uint16_t *embed = nullptr, *lm_head = nullptr;
+  float* ones = nullptr;  // all norm weights are 1
+  struct Layer {
+    uint16_t *wqkv, *wo, *wgu, *wd;
+    float* bqkv;
+  };
+  std::vector<Layer> layers;
+
+  // workspace
+  float* h = nullptr;
+  uint16_t *a = nullptr, *qkv = nullptr, *q = nullptr, *k = nullptr, *vt = nullptr;
+  uint16_t *attn = nullptr, *u = nullptr, *logits = nullptr;
+  float *rope_cos = nullptr, *rope_sin = nullptr;
+  int32_t* tickets = nullptr;
+  int num_cus = 256;
+  float* splitk_ws = nullptr;
+  int32_t* splitk_cnt = nullptr;
+  // decode state owned for cora_block_decode
+  int32_t *s_tokens = nullptr, *s_prev = nullptr, *s_persist = nullptr, *s_block = nullptr;
+  int32_t *s_step = nullptr, *s_top1 = nullptr, *s_done = nullptr, *s_passes = nullptr;
+  uint8_t *s_unres = nullptr, *s_decision = nullptr;
+  float* s_conf = nullptr;
+  int32_t* h_block = nullptr;  // pinned host mirror of block_idx
+
+  // gate/up GEMM timing
+  bool timing = false;
+  std::vector<hipEvent_t> ev;  // pairs
+  size_t ev_used = 0;
+  double acc_ms = 0.0;
+  int64_t launches = 0;
+};
+
+static cora_status validate_cfg(const cora_model_cfg& c) {
+  if (c.n_layers < 0 || c.d_model <= 0 || c.n_heads <= 0 || c.n_kv_heads <= 0 ||
+      c.ffn_dim <= 0 || c.vocab < 2)
+    return fail(CORA_ERR_INVALID_ARG, "model dimensions must be positive (vocab >= 2)");
+  if (c.mask_id < 0 || c.mask_id >= c.vocab)
+    return fail(CORA_ERR_INVALID_ARG, "mask_id must lie in [0, vocab)");
+  if (c.head_dim != 64 && c.head_dim != 128)
+    return fail(CORA_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
+  if (c.n_heads % c.n_kv_heads != 0)
+    return fail(CORA_ERR_UNSUPPORTED, "n_heads must be a multiple of n_kv_heads");
+  if (c.d_model % 64 != 0 || (c.n_heads * c.head_dim) % 64 != 0)
+    return fail(CORA_ERR_UNSUPPORTED, "d_model and n_heads*head_dim must be multiples of 64");
+  if (!(c.rms_eps > 0.f) || !(c.rope_theta > 0.f) || !isfinite(c.logit_scale) ||
+      !(c.init_std >= 0.0))
+    return fail(CORA_ERR_INVALID_ARG, "rms_eps, rope_theta must be > 0; logit_scale finite");
+  return CORA_OK;
+}
+
+static hipStream_t S(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+// ---------------------------------------------------------------------------------------
+extern "C" const char* cora_last_error(void) { return g_err.c_str(); }
+
+extern "C" cora_status cora_model_destroy(cora_model* m) {
+  if (!m) return CORA_OK;
+  for (hipEvent_t e : m->ev) (void)hipEventDestroy(e);
+  if (m->h_block) (void)hipHostFree(m->h_block);
+  if (m->ws_mem) (void)hipFree(m->ws_mem);
+  if (m->weight_mem) (void)hipFree(m->weight_mem);
+  delete m;
+  return CORA_OK;
+}
+
+extern "C" cora_status cora_model_create(const cora_model_cfg* cfg, uint64_t seed,
+                                         int32_t max_batch, int32_t max_seq, void* hip_stream,
+                                         cora_model** out) {
+  if (!cfg || !out) return fail(CORA_ERR_INVALID_ARG, "null cfg or out");
+  if (cora_status st = validate_cfg(*cfg)) return st;
+  if (max_batch <= 0 || max_seq <= 0) return fail(CORA_ERR_INVALID_ARG, "max_batch/max_seq <= 0");
+  const hipStream_t s = S(hip_stream);
+  cora_model* m = new cora_model();
+  m->cfg = *cfg;
+  m->max_batch = max_batch;
+  m->max_seq = max_seq;
+  m->max_seq_pad = round_up(max_seq, 64);
+  m->max_rows = max_seq < CORA_MAX_BLOCK_LEN ? max_seq : CORA_MAX_BLOCK_LEN;
+  const int d = cfg->d_model, V = cfg->vocab, hd = cfg->head_dim;
+  m->hq = cfg->n_heads * hd;
+  m->hkv = cfg->n_kv_heads * hd;
+  m->qkv_n = m->hq + 2 * m->hkv;
+  m->f_pad = round_up(cfg->ffn_dim, 64);
+  const int64_t L_ = cfg->n_layers;
+
+  // ---- weights
+  size_t wb = 2 * align_up((size_t)V * d * 2) + align_up((size_t)d * 4);
+  const size_t per_layer = align_up((size_t)m->qkv_n * d * 2) + align_up((size_t)d * m->hq * 2) +
+                           align_up((size_t)2 * m->f_pad * d * 2) +
+                           align_up((size_t)d * m->f_pad * 2) +
+                           (cfg->qkv_bias ? align_up((size_t)m->qkv_n * 4) : 0);
+  wb += per_layer * L_;
+  // ---- workspace
+  const size_t M = (size_t)max_batch * max_seq;
+  const size_t Ms = (size_t)max_batch * m->max_seq_pad;
+  const size_t rows = (size_t)max_batch * m->max_rows;
+  const size_t BL = M;
+  {
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+        cus > 0)
+      m->num_cus = cus;
+  }
+  const size_t skw = gemm_ws_floats_bound(m->num_cus);
+  size_t wsb = align_up(skw * 4) + align_up((size_t)m->num_cus * 4) + align_up(M * d * 4) + align_up(M * (size_t)(d > m->hq ? d : m->hq) * 2) +
+               align_up(M * m->qkv_n * 2) + align_up(Ms * m->hq * 2) + 2 * align_up(Ms * m->hkv * 2) +
+               align_up(M * m->hq * 2) + align_up(M * m->f_pad * 2) + align_up(rows * V * 2) +
+               2 * align_up((size_t)m->max_seq_pad * (hd / 2) * 4) + align_up(max_batch * 4) +
+               // decode state
+               align_up(BL * 4) * 3 + align_up(BL) + align_up(max_batch * 4) * 3 +
+               align_up(rows * 4) * 2 + align_up(rows) + align_up((size_t)max_batch * max_seq * 4);
+  hipError_t e = hipMalloc(&m->weight_mem, wb);
+  if (e != hipSuccess) {
+    cora_model_destroy(m);
+    return fail(e == hipErrorOutOfMemory ? CORA_ERR_OOM : CORA_ERR_HIP,
+                std::string("weight allocation: ") + hipGetErrorString(e));
+  }
+  e = hipMalloc(&m->ws_mem, wsb);
+  if (e != hipSuccess) {
+    cora_model_destroy(m);
+    return fail(e == hipErrorOutOfMemory ? CORA_ERR_OOM : CORA_ERR_HIP,
+                std::string("workspace allocation: ") + hipGetErrorString(e));
+  }
+  m->weight_bytes = wb;
+  m->ws_bytes = wsb;
+
+  Arena w{(char*)m->weight_mem, 0, wb};
+  m->embed = w.take<uint16_t>((size_t)V * d);
+  m->lm_head = w.take<uint16_t>((size_t)V * d);
+  m->ones = w.take<float>(d);
+  m->layers.resize(L_);
+  for (auto& ly : m->layers) {
+    ly.wqkv = w.take<uint16_t>((size_t)m->qkv_n * d);
+    ly.wo = w.take<uint16_t>((size_t)d * m->hq);
+    ly.wgu = w.take<uint16_t>((size_t)2 * m->f_pad * d);
+    ly.wd = w.take<uint16_t>((size_t)d * m->f_pad);
+    ly.bqkv = cfg->qkv_bias ? w.take<float>(m->qkv_n) : nullptr;
+  }
+  Arena a{(char*)m->ws_mem, 0, wsb};
+  m->splitk_ws = a.take<float>(skw);
+  m->splitk_cnt = a.take<int32_t>(m->num_cus);
+  m->h = a.take<float>(M * d);
+  m->a = a.take<uint16_t>(M * (d > m->hq ? d : m->hq));
+  m->qkv = a.take<uint16_t>(M * m->qkv_n);
+  m->q = a.take<uint16_t>(Ms * m->hq);
+  m->k = a.take<uint16_t>(Ms * m->hkv);
+  m->vt = a.take<uint16_t>(Ms * m->hkv);
+  m->attn = a.take<uint16_t>(M * m->hq);
+  m->u = a.take<uint16_t>(M * m->f_pad);
+  m->logits = a.take<uint16_t>(rows * V);
+  m->rope_cos = a.take<float>((size_t)m->max_seq_pad * (hd / 2));
+  m->rope_sin = a.take<float>((size_t)m->max_seq_pad * (hd / 2));
+  m->tickets = a.take<int32_t>(max_batch);
+  m->s_tokens = a.take<int32_t>(BL);
+  m->s_prev = a.take<int32_t>(BL);
+  m->s_persist = a.take<int32_t>(BL);
+  m->s_unres = a.take<uint8_t>(BL);
+  m->s_block = a.take<int32_t>(max_batch);
+  m->s_step = a.take<int32_t>(max_batch);
+  m->s_done = a.take<int32_t>(max_batch);
+  m->s_top1 = a.take<int32_t>(rows);
+  m->s_conf = a.take<float>(rows);
+  m->s_decision = a.take<uint8_t>(rows);
+  m->s_passes = a.take<int32_t>((size_t)max_batch * max_seq);
+  e = hipHostMalloc((void**)&m->h_block, max_batch * sizeof(int32_t), hipHostMallocDefault);
+  if (e != hipSuccess) {
+    cora_model_destroy(m);
+    return fail(CORA_ERR_HIP, std::string("pinned allocation: ") + hipGetErrorString(e));
+  }
+
+  // ---- fill weights
+  auto st = [&]() -> cora_status {
+    HIP_TRY(hipMemsetAsync(m->weight_mem, 0, wb, s));
+    HIP_TRY(hipMemsetAsync(m->tickets, 0, max_batch * sizeof(int32_t), s));
+    HIP_TRY(hipMemsetAsync(m->splitk_cnt, 0, m->num_cus * sizeof(int32_t), s));
+    const double sd = cfg->init_std;
+    HIP_TRY(launch_init_bf16(m->embed, seed, 1, V, d, d, ROW_IDENTITY, 0, sd, s));
+    HIP_TRY(launch_init_bf16(m->lm_head, seed, 2, V, d, d, ROW_IDENTITY, 0, sd, s));
+    HIP_TRY(launch_fill_f32(m->ones, 1.0f, d, s));
+    for (int l = 0; l < (int)L_; ++l) {
+      const auto& ly = m->layers[l];
+      const uint64_t t0 = 100 + 16 * (uint64_t)l;
+      HIP_TRY(launch_init_bf16(ly.wqkv, seed, t0 + 0, m->hq, d, d, ROW_IDENTITY, 0, sd, s));
+      HIP_TRY(launch_init_bf16(ly.wqkv, seed, t0 + 1, m->hkv, d, d, ROW_IDENTITY, m->hq, sd, s));
+      HIP_TRY(launch_init_bf16(ly.wqkv, seed, t0 + 2, m->hkv, d, d, ROW_IDENTITY, m->hq + m->hkv,
+                               sd, s));
+      HIP_TRY(launch_init_bf16(ly.wo, seed, t0 + 3, d, m->hq, m->hq, ROW_IDENTITY, 0, sd, s));
+      HIP_TRY(launch_init_bf16(ly.wgu, seed, t0 + 4, cfg->ffn_dim, d, d, ROW_GATE, 0, sd, s));
+      HIP_TRY(launch_init_bf16(ly.wgu, seed, t0 + 5, cfg->ffn_dim, d, d, ROW_UP, 0, sd, s));
+      HIP_TRY(launch_init_bf16(ly.wd, seed, t0 + 6, d, cfg->ffn_dim, m->f_pad, ROW_IDENTITY, 0, sd,
+                               s));
+      if (cfg->qkv_bias) {
+        HIP_TRY(launch_init_f32(ly.bqkv, seed, t0 + 7, m->hq, sd, s));
+        HIP_TRY(launch_init_f32(ly.bqkv + m->hq, seed, t0 + 8, m->hkv, sd, s));
+        HIP_TRY(launch_init_f32(ly.bqkv + m->hq + m->hkv, seed, t0 + 9, m->hkv, sd, s));
+      }
+    }
+    // RoPE tables in fp64, stored fp32: angle = pos * theta^(-2j/hd)
+    const int half = hd / 2;
+    std::vector<float> cs((size_t)m->max_seq_pad * half), sn(cs.size());
+    for (int p = 0; p < m->max_seq_pad; ++p)
+      for (int j = 0; j < half; ++j) {
+        const double ang = (double)p * pow((double)cfg->rope_theta, -2.0 * j / hd);
+        cs[(size_t)p * half + j] = (float)cos(ang);
+        sn[(size_t)p * half + j] = (float)sin(ang);
+      }
+    HIP_TRY(hipMemcpyAsync(m->rope_cos, cs.data(), cs.size() * 4, hipMemcpyHostToDevice, s));
+    HIP_TRY(hipMemcpyAsync(m->rope_sin, sn.data(), sn.size() * 4, hipMemcpyHostToDevice, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    return CORA_OK;
+  }();
+  if (st != CORA_OK) {
+    cora_model_destroy(m);
+    return st;
+  }
+  *out = m;
+  return CORA_OK;
+}
+
+extern "C" cora_status cora_model_device_bytes(cora_model* m, size_t* wbytes, size_t* wsbytes) {
+  if (!m) return fail(CORA_ERR_INVALID_ARG, "null model");
+  if (wbytes) *wbytes = m->weight_bytes;
+  if (wsbytes) *wsbytes = m->ws_bytes;
+  return CORA_OK;
+}
+
+// ---- timing ------------------------------------------------------------------------------
+extern "C" cora_status cora_model_set_timing(cora_model* m, int32_t enable) {
+  if (!m) return fail(CORA_ERR_INVALID_ARG, "null model");
+  m->timing = enable != 0;
+  m->ev_used = 0;
+  m->acc_ms = 0.0;
+  m->launches = 0;
+  return CORA_OK;
+}
+
+static cora_status drain_events(cora_model* m) {
+  for (size_t i = 0; i + 1 < m->ev_used; i += 2) {
+    HIP_TRY(hipEventSynchronize(m->ev[i + 1]));
+    float ms = 0.f;
+    HIP_TRY(hipEventElapsedTime(&ms, m->ev[i], m->ev[i + 1]));
+    m->acc_ms += ms;
+    m->launches += 1;
+  }
+  m->ev_used = 0;
+  return CORA_OK;
+}
+
+extern "C" cora_status cora_model_read_timing(cora_model* m, double* total_ms, int64_t* launches) {
+  if (!m) return fail(CORA_ERR_INVALID_ARG, "null model");
+  if (cora_status st = drain_events(m)) return st;
+  if (total_ms) *total_ms = m->acc_ms;
+  if (launches) *launches = m->launches;
+  return CORA_OK;
+}
+
+static cora_status timed_event(cora_model* m, hipStream_t s) {
+  if (m->ev_used == m->ev.size()) {
+    if (m->ev.size() >= 8192) {
+      if (cora_status st = drain_events(m)) return st;
+    } else {
+      for (int i = 0; i < 64; ++i) {
+        hipEvent_t e;
+        HIP_TRY(hipEventCreate(&e));
+        m->ev.push_back(e);
+      }
+    }
+  }
+  HIP_TRY(hipEventRecord(m->ev[m->ev_used++], s));
+  return CORA_OK;
+}
+
+// ---- one dense pass ----------------------------------------------------------------------
+static cora_status gemm(cora_model* m, int epi, const GemmArgs& g, hipStream_t s) {
+  const GemmPlan p = gemm_plan(epi, g.M, g.N, g.K, m->num_cus);
+  GemmArgs a = g;
+  a.ws = m->splitk_ws;
+  a.counters = m->splitk_cnt;
+  HIP_TRY(launch_gemm(epi, a, p, s));
+  return CORA_OK;
+}
+
+static cora_status run_layers(cora_model* m, const int32_t* tokens, int B, int L, hipStream_t s) {
+  const auto& c = m->cfg;
+  const int d = c.d_model, M = B * L, Ls = round_up(L, 64);
+  HIP_TRY(launch_embed(tokens, m->embed, m->h, M, d, c.vocab, s));
+  const RowSel all{0, L, 0, 0, 0, 0, 0, nullptr};
+  for (const auto& ly : m->layers) {
+    HIP_TRY(launch_rmsnorm(m->h, m->ones, m->a, M, d, c.rms_eps, all, s));
+    GemmArgs g{m->a, d, ly.wqkv, d, M, m->qkv_n, d, m->qkv, m->qkv_n, ly.bqkv, 1.0f};
+    if (cora_status st = gemm(m, EPI_BF16, g, s)) return st;
+    HIP_TRY(launch_rope_split(m->qkv, m->q, m->k, m->vt, m->rope_cos, m->rope_sin, B, L, Ls,
+                              c.n_heads, c.n_kv_heads, c.head_dim, s));
+    HIP_TRY(launch_attention(m->q, m->k, m->vt, m->attn, B, L, Ls, c.n_heads, c.n_kv_heads,
+                             c.head_dim, s));
+    g = GemmArgs{m->attn, m->hq, ly.wo, m->hq, M, d, m->hq, m->h, d, nullptr, 1.0f};
+    if (cora_status st = gemm(m, EPI_ADD_F32, g, s)) return st;
+    HIP_TRY(launch_rmsnorm(m->h, m->ones, m->a, M, d, c.rms_eps, all, s));
+    g = GemmArgs{m->a, d, ly.wgu, d, M, 2 * m->f_pad, d, m->u, m->f_pad, nullptr, 1.0f};
+    if (m->timing)
+      if (cora_status st = timed_event(m, s)) return st;
+    if (cora_status st = gemm(m, EPI_SWIGLU, g, s)) return st;
+    if (m->timing)
+      if (cora_status st = timed_event(m, s)) return st;
+    g = GemmArgs{m->u, m->f_pad, ly.wd, m->f_pad, M, d, m->f_pad, m->h, d, nullptr, 1.0f};
+    if (cora_status st = gemm(m, EPI_ADD_F32, g, s)) return st;
+  }
+  return CORA_OK;
+}
+
+static cora_status lm_head(cora_model* m, const RowSel& sel, int n_out_rows, uint16_t* logits,
+                           hipStream_t s) {
+  const auto& c = m->cfg;
+  HIP_TRY(launch_rmsnorm(m->h, m->ones, m->a, n_out_rows, c.d_model, c.rms_eps, sel, s));
+  GemmArgs g{m->a, c.d_model, m->lm_head, c.d_model, n_out_rows, c.vocab, c.d_model, logits,
+             c.vocab, nullptr, c.logit_scale};
+  return gemm(m, EPI_BF16, g, s);
+}
+
+extern "C" cora_status cora_forward_logits(cora_model* m, const int32_t* d_tokens, int32_t B,
+                                           int32_t L, int32_t row_begin, int32_t n_rows,
+                                           uint16_t* d_logits, void* hip_stream) {
+  if (!m || !d_tokens || !d_logits) return fail(CORA_ERR_INVALID_ARG, "null argument");
+  if (B <= 0 || L <= 0 || B > m->max_batch || L > m->max_seq)
+    return fail(CORA_ERR_INVALID_ARG, "B/L outside [1, max_batch] x [1, max_seq]");
+  if (row_begin < 0 || n_rows < 0 || row_begin + n_rows > L)
+    return fail(CORA_ERR_INVALID_ARG, "rows outside the canvas");
+  if (n_rows == 0) return CORA_OK;
+  const hipStream_t s = S(hip_stream);
+  if (cora_status st = run_layers(m, d_tokens, B, L, s)) return st;
+  const RowSel sel{1, L, n_rows, row_begin, 0, 0, 0, nullptr};
+  return lm_head(m, sel, B * n_rows, d_logits, s);
+}
+
+// ---- decision rules ----------------------------------------------------------------------
+static cora_status check_sched_gate(const cora_sched_cfg* sc, const cora_gate_cfg* gt) {
+  if (!sc || !gt) return fail(CORA_ERR_INVALID_ARG, "null sched or gate");
+  if (sc->block_len < 1 || sc->block_len > CORA_MAX_BLOCK_LEN)
+    return fail(CORA_ERR_UNSUPPORTED, "block_len must lie in [1, 256]");
+  if (sc->steps_per_block < 1 || sc->steps_per_block > sc->block_len)
+    return fail(CORA_ERR_INVALID_ARG, "steps_per_block must lie in [1, block_len]");
+  if (gt->persist_scope != 0)
+    return fail(CORA_ERR_UNSUPPORTED, "only the BLOCK persistence scope is implemented");
+  if (gt->m_req < 0 || isnan(gt->delta_p))
+    return fail(CORA_ERR_INVALID_ARG, "m_req must be >= 0 and delta_p a number");
+  return CORA_OK;
+}
+
+static cora_status check_state(const cora_state* st, const cora_sched_cfg* sc) {
+  if (!st) return fail(CORA_ERR_INVALID_ARG, "null state");
+  if (!st->tokens || !st->unresolved || !st->prev_top1 || !st->persist || !st->block_idx ||
+      !st->step_idx || !st->top1 || !st->conf || !st->decision || !st->done)
+    return fail(CORA_ERR_INVALID_ARG, "null state array");
+  if (st->B <= 0 || st->prompt_len < 0 || st->gen_len <= 0 || st->gen_len % sc->block_len != 0)
+    return fail(CORA_ERR_INVALID_ARG, "B > 0, prompt_len >= 0, gen_len a positive multiple "
+                                      "of block_len");
+  return CORA_OK;
+}
+
+static VocabGateArgs vg_args(const uint16_t* logits, int n_rows, int row_begin, int V,
+                             int mask_id, const cora_state* st, int k_transfer,
+                             const cora_sched_cfg* sc, const cora_gate_cfg* gt, int32_t* tickets) {
+  VocabGateArgs a{};
+  a.logits = logits; a.n_rows = n_rows; a.row_begin = row_begin; a.V = V; a.mask_id = mask_id;
+  a.tokens = st->tokens; a.unresolved = st->unresolved; a.prev_top1 = st->prev_top1;
+  a.persist = st->persist; a.block_idx = st->block_idx; a.step_idx = st->step_idx;
+  a.top1 = st->top1; a.conf = st->conf; a.decision = st->decision; a.done = st->done;
+  a.passes = st->passes;
+  a.B = st->B; a.L = st->prompt_len + st->gen_len; a.prompt_len = st->prompt_len;
+  a.block_len = sc->block_len; a.steps_per_block = sc->steps_per_block;
+  a.n_blocks = st->gen_len / sc->block_len;
+  a.k_transfer = k_transfer;
+  a.delta_p = gt->delta_p; a.m_req = gt->m_req; a.gate_enabled = gt->gate_enabled ? 1 : 0;
+  a.tickets = tickets;
+  return a;
+}
+
+extern "C" size_t cora_vocab_gate_workspace_bytes(int32_t B) {
+  return align_up((size_t)(B > 0 ? B : 0) * sizeof(int32_t));
+}
+
+extern "C" cora_status cora_vocab_gate(const uint16_t* d_logits, int32_t n_rows, int32_t row_begin,
+                                       int32_t V, int32_t mask_id, cora_state* st,
+                                       int32_t k_transfer, const cora_sched_cfg* sc,
+                                       const cora_gate_cfg* gt, void* d_workspace,
+                                       size_t workspace_bytes, void* hip_stream) {
+  if (cora_status e = check_sched_gate(sc, gt)) return e;
+  if (cora_status e = check_state(st, sc)) return e;
+  if (!d_logits || !d_workspace) return fail(CORA_ERR_INVALID_ARG, "null logits or workspace");
+  if (V < 2 || mask_id < 0 || mask_id >= V) return fail(CORA_ERR_INVALID_ARG, "bad V/mask_id");
+  if (workspace_bytes < cora_vocab_gate_workspace_bytes(st->B))
+    return fail(CORA_ERR_INVALID_ARG, "workspace too small");
+  const int L = st->prompt_len + st->gen_len;
+  if (row_begin >= 0) {
+    if (row_begin > st->prompt_len || row_begin + n_rows < L || row_begin + n_rows > L)
+      return fail(CORA_ERR_INVALID_ARG, "fixed rows must cover the generation region and stay "
+                                        "inside the canvas");
+  } else if (n_rows != sc->block_len) {
+    return fail(CORA_ERR_INVALID_ARG, "block-following rows need n_rows == block_len");
+  }
+  if (n_rows <= 0) return fail(CORA_ERR_INVALID_ARG, "n_rows must be positive");
+  const VocabGateArgs a = vg_args(d_logits, n_rows, row_begin, V, mask_id, st, k_transfer, sc, gt,
+                                  reinterpret_cast<int32_t*>(d_workspace));
+  HIP_TRY(launch_vocab_gate(a, S(hip_stream)));
+  return CORA_OK;
+}
+
+static cora_status denoise_step(cora_model* m, cora_state* st, const cora_sched_cfg* sc,
+                                const cora_gate_cfg* gt, hipStream_t s) {
+  const int B = st->B, L = st->prompt_len + st->gen_len, blk = sc->block_len;
+  if (cora_status e = run_layers(m, st->tokens, B, L, s)) return e;
+  const RowSel sel{2, L, blk, 0, st->prompt_len, blk, st->gen_len / blk, st->block_idx};
+  if (cora_status e = lm_head(m, sel, B * blk, m->logits, s)) return e;
+  const VocabGateArgs a = vg_args(m->logits, blk, -1, m->cfg.vocab, m->cfg.mask_id, st, -1, sc,
+                                  gt, m->tickets);
+  HIP_TRY(launch_vocab_gate(a, s));
+  return CORA_OK;
+}
+
+static cora_status check_step(cora_model* m, const cora_state* st, const cora_sched_cfg* sc,
+                              const cora_gate_cfg* gt) {
+  if (!m) return fail(CORA_ERR_INVALID_ARG, "null model");
+  if (cora_status e = check_sched_gate(sc, gt)) return e;
+  if (cora_status e = check_state(st, sc)) return e;
+  if (st->B > m->max_batch || st->prompt_len + st->gen_len > m->max_seq)
+    return fail(CORA_ERR_INVALID_ARG, "state exceeds the model's max_batch / max_seq");
+  if (sc->block_len > m->max_rows)
+    return fail(CORA_ERR_INVALID_ARG, "block_len exceeds the model's row workspace");
+  return CORA_OK;
+}
+
+extern "C" cora_status cora_denoise_step(cora_model* m, cora_state* st, const cora_sched_cfg* sc,
+                                         const cora_gate_cfg* gt, void* hip_stream) {
+  if (cora_status e = check_step(m, st, sc, gt)) return e;
+  return denoise_step(m, st, sc, gt, S(hip_stream));
+}
+
+extern "C" cora_status cora_block_decode(cora_model* m, const int32_t* d_prompt, int32_t B,
+                                         int32_t prompt_len, int32_t gen_len,
+                                         const cora_sched_cfg* sc, const cora_gate_cfg* gt,
+                                         int32_t* d_out_tokens, int32_t* h_passes,
+                                         int32_t* h_total_passes, void* hip_stream) {
+  if (!m || !d_out_tokens || !h_passes || (prompt_len > 0 && !d_prompt))
+    return fail(CORA_ERR_INVALID_ARG, "null argument");
+  const hipStream_t s = S(hip_stream);
+  cora_state st{m->s_tokens, m->s_unres, m->s_prev, m->s_persist, m->s_block, m->s_step,
+                m->s_top1, m->s_conf, m->s_decision, m->s_done, m->s_passes,
+                B, prompt_len, gen_len};
+  if (cora_status e = check_step(m, &st, sc, gt)) return e;
+  const int n_blocks = gen_len / sc->block_len, L = prompt_len + gen_len;
+  HIP_TRY(launch_state_init(d_prompt, B, prompt_len, gen_len, m->cfg.mask_id, st.tokens,
+                            st.unresolved, st.prev_top1, st.persist, st.block_idx, st.step_idx,
+                            st.passes, n_blocks, s));
+  const int64_t max_passes = (int64_t)n_blocks * sc->steps_per_block;
+  int64_t total = 0;
+  for (;;) {
+    if (cora_status e = denoise_step(m, &st, sc, gt, s)) return e;
+    ++total;
+    HIP_TRY(hipMemcpyAsync(m->h_block, st.block_idx, B * sizeof(int32_t), hipMemcpyDeviceToHost,
+                           s));
+    HIP_TRY(hipStreamSynchronize(s));
+    bool all = true;
+    for (int b = 0; b < B; ++b) all = all && m->h_block[b] >= n_blocks;
+    if (all) break;
+    if (total > max_passes)
+      return fail(CORA_ERR_STATE, "decode did not terminate within the dense horizon");
+  }
+  HIP_TRY(hipMemcpyAsync(d_out_tokens, st.tokens, (size_t)B * L * sizeof(int32_t),
+                         hipMemcpyDeviceToDevice, s));
+  HIP_TRY(hipMemcpyAsync(h_passes, st.passes, (size_t)B * n_blocks * sizeof(int32_t),
+                         hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  if (h_total_passes) *h_total_passes = (int32_t)total;
+  return CORA_OK;
+}
+
+// ---- weight read-back in logical [out, in] layout ---------------------------------------
+extern "C" cora_status cora_model_copy_tensor(cora_model* m, int32_t tensor_id, void* h_dst,
+                                              size_t bytes) {
+  if (!m || !h_dst) return fail(CORA_ERR_INVALID_ARG, "null argument");
+  const auto& c = m->cfg;
+  const int d = c.d_model;
+  auto want = [&](size_t n) -> cora_status {
+    return bytes == n * 2 ? CORA_OK
+                          : fail(CORA_ERR_INVALID_ARG, "bytes does not match the tensor size");
+  };
+  if (tensor_id == 1 || tensor_id == 2) {
+    if (cora_status e = want((size_t)c.vocab * d)) return e;
+    HIP_TRY(hipMemcpy(h_dst, tensor_id == 1 ? m->embed : m->lm_head, bytes, hipMemcpyDeviceToHost));
+    return CORA_OK;
+  }
+  if (tensor_id < 100) return fail(CORA_ERR_INVALID_ARG, "unknown tensor id");
+  const int l = (tensor_id - 100) / 16, j = (tensor_id - 100) % 16;
+  if (l >= c.n_layers) return fail(CORA_ERR_INVALID_ARG, "layer out of range");
+  const auto& ly = m->layers[l];
+  uint16_t* out = reinterpret_cast<uint16_t*>(h_dst);
+  switch (j) {
+    case 0: case 1: case 2: {
+      const int rows = j == 0 ? m->hq : m->hkv;
+      const int off = j == 0 ? 0 : (j == 1 ? m->hq : m->hq + m->hkv);
+      if (cora_status e = want((size_t)rows * d)) return e;
+      HIP_TRY(hipMemcpy(h_dst, ly.wqkv + (size_t)off * d, bytes, hipMemcpyDeviceToHost));
+      return CORA_OK;
+    }
+    case 3:
+      if (cora_status e = want((size_t)d * m->hq)) return e;
+      HIP_TRY(hipMemcpy(h_dst, ly.wo, bytes, hipMemcpyDeviceToHost));
+      return CORA_OK;
+    case 4: case 5: {
+      const int F = c.ffn_dim;
+      if (cora_status e = want((size_t)F * d)) return e;
+      std::vector<uint16_t> tmp((size_t)2 * m->f_pad * d);
+      HIP_TRY(hipMemcpy(tmp.data(), ly.wgu, tmp.size() * 2, hipMemcpyDeviceToHost));
+      for (int r = 0; r < F; ++r) {
+        const size_t pr = (size_t)(r >> 5) * 64 + (j == 5 ? 32 : 0) + (r & 31);
+        memcpy(out + (size_t)r * d, tmp.data() + pr * d, (size_t)d * 2);
+      }
+      return CORA_OK;
+    }
+    case 6:
+      if (cora_status e = want((size_t)d * c.ffn_dim)) return e;
+      HIP_TRY(hipMemcpy2D(h_dst, (size_t)c.ffn_dim * 2, ly.wd, (size_t)m->f_pad * 2,
+                          (size_t)c.ffn_dim * 2, d, hipMemcpyDeviceToHost));
+      return CORA_OK;
+    case 7: case 8: case 9: {
+      if (!c.qkv_bias) return fail(CORA_ERR_INVALID_ARG, "model has no qkv bias");
+      const int n = j == 7 ? m->hq : m->hkv;
+      const int off = j == 7 ? 0 : (j == 8 ? m->hq : m->hq + m->hkv);
+      if (cora_status e = want((size_t)n)) return e;
+      std::vector<float> tmp(n);
+      HIP_TRY(hipMemcpy(tmp.data(), ly.bqkv + off, (size_t)n * 4, hipMemcpyDeviceToHost));
+      for (int i = 0; i < n; ++i) {
+        uint32_t u;
+        memcpy(&u, &tmp[i], 4);
+        out[i] = (uint16_t)(u >> 16);
+      }
+      return CORA_OK;
+    }
+  }
+  return fail(CORA_ERR_INVALID_ARG, "unknown tensor id");
+}
