@@ -5,10 +5,10 @@
 // of WAVES_M x WAVES_N wavefronts owns a BM x BN tile; each wavefront owns
 // TM x TN blocks of 32 x 32 computed with v_mfma_f32_32x32x16_bf16.
 //
-// Pipeline: two BK-slices are in flight in registers while a third is multiplied out
-// of LDS (two LDS buffers, one barrier per slice), so a slice's global loads have two
-// slices of MFMA work to arrive.  LDS rows are padded by 16 bytes so the 32 lanes that
-// read one fragment column hit distinct banks.
+// Pipeline: the next BK-slice (DEPTH 1) or the next two (DEPTH 2) are in flight in
+// registers while the current one is multiplied out of LDS (two LDS buffers, one barrier
+// per slice).  LDS rows are padded by 16 bytes so the lanes that read one fragment
+// column hit distinct banks.
 //
 // Split-K (for outputs with too few tiles to fill the chip): split s of a tile
 // accumulates K-slices [s*nk, (s+1)*nk), stores its fp32 partial tile to a workspace,
@@ -40,7 +40,7 @@ __device__ __forceinline__ void buf_load(u32x4_t (&r)[N], __amdgpu_buffer_rsrc_t
     r[i] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, voff, i * step, 0));
 }
 
-template <int WAVES_M, int WAVES_N, int TM, int TN, int EPI>
+template <int WAVES_M, int WAVES_N, int TM, int TN, int EPI, int DEPTH>
 __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void k_gemm(GemmArgs g) {
   constexpr int NT = WAVES_M * WAVES_N * 64;
   constexpr int BM = WAVES_M * TM * 32, BN = WAVES_N * TN * 32;
@@ -48,7 +48,7 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void k_gemm(GemmArgs g) {
   constexpr int CB = BN * BK / 8 / NT;
   constexpr int NACC = TM * TN * 16;    // accumulators per thread
   static_assert(CA * NT * 8 == BM * BK && CB * NT * 8 == BN * BK, "tile/thread mismatch");
-  static_assert(EPI != EPI_SWIGLU || TN == 2, "SwiGLU epilogue pairs two 32-column blocks");
+  static_assert(EPI != EPI_SWIGLU || TN % 2 == 0, "SwiGLU epilogue pairs 32-column blocks");
 
   __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * LDK];
   __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BN * LDK];
@@ -89,7 +89,8 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void k_gemm(GemmArgs g) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-  u32x4_t ra0[CA], rb0[CB], ra1[CA], rb1[CB];
+  u32x4_t ra0[CA], rb0[CB];
+  [[maybe_unused]] u32x4_t ra1[CA], rb1[CB];
 #define GEMM_FETCH(ra, rb, kt)                                   \
   do {                                                           \
     buf_load<CA>(ra, a_rs, a_off + (kt) * BK * 2, a_step);       \
@@ -140,82 +141,109 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void k_gemm(GemmArgs g) {
     mfmas(fa1, fb1);
   };
 
-  // slices kt (LDS), kt+1 and kt+2 (registers) in flight
-  GEMM_FETCH(ra0, rb0, 0);
-  if (nk > 1) GEMM_FETCH(ra1, rb1, 1);
-  stash(0, ra0, rb0);
-  __syncthreads();
-  int kt = 0;
-  for (; kt + 1 < nk; kt += 2) {
-    if (kt + 2 < nk) GEMM_FETCH(ra0, rb0, kt + 2);
-    compute(0);
-    stash(1, ra1, rb1);
+  if constexpr (DEPTH == 2) {
+    // slices kt (LDS), kt+1 and kt+2 (registers) in flight
+    GEMM_FETCH(ra0, rb0, 0);
+    if (nk > 1) GEMM_FETCH(ra1, rb1, 1);
+    stash(0, ra0, rb0);
     __syncthreads();
-    if (kt + 3 < nk) GEMM_FETCH(ra1, rb1, kt + 3);
-    compute(1);
-    if (kt + 2 < nk) stash(0, ra0, rb0);
+    int kt = 0;
+    for (; kt + 1 < nk; kt += 2) {
+      if (kt + 2 < nk) GEMM_FETCH(ra0, rb0, kt + 2);
+      compute(0);
+      stash(1, ra1, rb1);
+      __syncthreads();
+      if (kt + 3 < nk) GEMM_FETCH(ra1, rb1, kt + 3);
+      compute(1);
+      if (kt + 2 < nk) stash(0, ra0, rb0);
+      __syncthreads();
+    }
+    if (kt < nk) compute(0);  // odd slice count: the last slice sits in buffer 0
+  } else {
+    // slice kt in LDS, slice kt+1 in registers
+    GEMM_FETCH(ra0, rb0, 0);
+    stash(0, ra0, rb0);
     __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+      if (kt + 1 < nk) GEMM_FETCH(ra0, rb0, kt + 1);
+      compute(kt & 1);
+      if (kt + 1 < nk) stash((kt + 1) & 1, ra0, rb0);
+      __syncthreads();
+    }
   }
-  if (kt < nk) compute(0);  // odd slice count: the last slice sits in buffer 0
 #undef GEMM_FETCH
   if (g.splits > 1) {
-    // deterministic split-K: partials laid out [tile][split][thread][NACC]
-    float* part = g.ws + ((int64_t)tile * g.splits) * NT * NACC;
-    float* mine = part + ((int64_t)split * NT + tid) * NACC;
+    // Deterministic split-K.  Partials of a tile are laid out [split][NACC/4][thread] as
+    // 16-byte vectors, so each store instruction covers 1 KiB contiguously.  They are
+    // written and read with agent-scope coherence (sc1) instead of a release fence, which
+    // would write back the whole L2: completed sc1 stores (vmcnt 0) are visible to any
+    // XCD, then the ticket is taken.
+    const int64_t part_floats = (int64_t)g.splits * NT * NACC;
+    const __amdgpu_buffer_rsrc_t ws_rs = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(g.ws + (int64_t)tile * part_floats), (short)0, (int)(part_floats * 4), 0x00020000);
+    constexpr int SC1 = 16;
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
       for (int j = 0; j < TN; ++j)
 #pragma unroll
-        for (int e = 0; e < 16; e += 4)
-          *reinterpret_cast<f32x4_t*>(mine + (i * TN + j) * 16 + e) =
-              f32x4_t{acc[i][j][e], acc[i][j][e + 1], acc[i][j][e + 2], acc[i][j][e + 3]};
-    __threadfence();
+        for (int e = 0; e < 16; e += 4) {
+          const int q = (i * TN + j) * 4 + e / 4;
+          const f32x4_t v{acc[i][j][e], acc[i][j][e + 1], acc[i][j][e + 2], acc[i][j][e + 3]};
+          __builtin_amdgcn_raw_buffer_store_b128(v, ws_rs, ((split * (NACC / 4) + q) * NT + tid) * 16,
+                                                 0, SC1);
+        }
+    __builtin_amdgcn_s_waitcnt(0);  // every counter drained: the partial stores completed
     __syncthreads();
-    if (tid == 0) s_last = atomicAdd(&g.counters[tile], 1) == g.splits - 1;
+    if (tid == 0)
+      s_last = __hip_atomic_fetch_add(&g.counters[tile], 1, __ATOMIC_RELAXED,
+                                      __HIP_MEMORY_SCOPE_AGENT) == g.splits - 1;
     __syncthreads();
     if (!s_last) return;
-    __threadfence();
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
       for (int j = 0; j < TN; ++j)
 #pragma unroll
         for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
-    for (int s = 0; s < g.splits; ++s) {
-      const float* p = part + ((int64_t)s * NT + tid) * NACC;
+    for (int sp = 0; sp < g.splits; ++sp) {
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j)
 #pragma unroll
           for (int e = 0; e < 16; e += 4) {
-            const f32x4_t v = *reinterpret_cast<const f32x4_t*>(p + (i * TN + j) * 16 + e);
+            const int q = (i * TN + j) * 4 + e / 4;
+            const f32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(
+                ws_rs, ((sp * (NACC / 4) + q) * NT + tid) * 16, 0, SC1);
             acc[i][j][e] += v[0];
             acc[i][j][e + 1] += v[1];
             acc[i][j][e + 2] += v[2];
             acc[i][j][e + 3] += v[3];
           }
     }
-    if (tid == 0) g.counters[tile] = 0;
+    if (tid == 0) __hip_atomic_store(&g.counters[tile], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 
   // epilogue: acc[i][j][e] is C[row, col] with
   //   row = m0 + wm*TM*32 + i*32 + 8*(e/4) + 4*(lane/32) + e%4,  col = n0 + wn*TN*32 + j*32 + lane%32
   const int col_l = lane & 31, row_q = (lane >> 5) * 4;
   if constexpr (EPI == EPI_SWIGLU) {
-    const int jcol = (n0 + wn * 64) / 2 + col_l;  // output (ffn) column
-    if (2 * (jcol - col_l) < g.N) {
-      uint16_t* C = reinterpret_cast<uint16_t*>(g.C);
+    uint16_t* C = reinterpret_cast<uint16_t*>(g.C);
+#pragma unroll
+    for (int t = 0; t < TN / 2; ++t) {
+      const int pcol = n0 + wn * TN * 32 + t * 64;  // 64 physical columns: 32 gate, 32 up
+      if (pcol >= g.N) continue;
+      const int jcol = pcol / 2 + col_l;            // output (ffn) column
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int row = m0 + wm * TM * 32 + i * 32 + 8 * (e >> 2) + row_q + (e & 3);
           if (row < g.M) {
-            const float gt = acc[i][0][e], up = acc[i][1][e];
-            const float s = gt / (1.0f + __expf(-gt));
-            C[(int64_t)row * g.ldc + jcol] = (uint16_t)f32_to_bf16_bits(s * up);
+            const float gt = acc[i][2 * t][e], up = acc[i][2 * t + 1][e];
+            const float sg = gt / (1.0f + __expf(-gt));
+            C[(int64_t)row * g.ldc + jcol] = (uint16_t)f32_to_bf16_bits(sg * up);
           }
         }
     }
@@ -244,39 +272,66 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void k_gemm(GemmArgs g) {
   }
 }
 
-// ---- tile configurations -------------------------------------------------------------
-enum GemmCfg { CFG_BIG = 0, CFG_SMALL_M = 1 };
-
-static void cfg_tile(int cfg, int epi, int* bm, int* bn) {
-  if (cfg == CFG_SMALL_M) { *bm = 32; *bn = epi == EPI_SWIGLU ? 128 : 128; return; }
-  *bm = 256; *bn = 128;
+// ---- tile configurations ---------------------------------------------------------------
+// LDS read throughput per CU grows with the number of resident waves (one wave per SIMD
+// cannot keep enough reads in flight to feed the MFMA pipe), so the large-tile configs
+// run 2-4 waves per SIMD with a single register stage.
+// cfg 0: 256 x 256 tile, 16 waves (4 x 4), wave tile 64 x 64
+// cfg 1:  32 x 128 tile, 4 waves (1 x 4) (2 waves for SwiGLU), for M <= 64 (LM head rows)
+// cfg 2: 256 x 128 tile,  8 waves (4 x 2), wave tile 64 x 64
+struct CfgShape { int bm, bn; };
+static CfgShape cfg_shape(int cfg) {
+  switch (cfg) {
+    case 0: return {256, 256};
+    case 1: return {32, 128};
+    default: return {256, 128};
+  }
 }
 
-GemmPlan gemm_plan(int epi, int M, int N, int K, int num_cus) {
+int gemm_num_cfgs() { return 3; }
+
+GemmPlan gemm_plan_cfg(int epi, int M, int N, int K, int num_cus, int cfg) {
   GemmPlan p{};
-  p.cfg = M <= 64 ? CFG_SMALL_M : CFG_BIG;
-  int bm, bn;
-  cfg_tile(p.cfg, epi, &bm, &bn);
-  p.tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
+  p.cfg = cfg;
+  const CfgShape sh = cfg_shape(cfg);
+  p.tiles = ((M + sh.bm - 1) / sh.bm) * ((N + sh.bn - 1) / sh.bn);
   p.splits = 1;
-  if (epi == EPI_ADD_F32 && p.cfg == CFG_BIG) {
+  if (cfg != 1 && epi == EPI_ADD_F32) {
     // split the K loop until the grid covers the chip, keeping >= 8 slices per split
     const int nk = K / BK;
     while (p.tiles * p.splits < num_cus && p.splits < 8 && nk % (p.splits * 2) == 0 &&
            nk / (p.splits * 2) >= 8)
       p.splits *= 2;
   }
-  const int nt = p.cfg == CFG_SMALL_M ? 256 : 256;
-  p.ws_floats = p.splits > 1 ? (size_t)p.tiles * p.splits * bm * bn : 0;
-  (void)nt;
+  p.ws_floats = p.splits > 1 ? (size_t)p.tiles * p.splits * sh.bm * sh.bn : 0;
   return p;
 }
 
-template <int WAVES_M, int WAVES_N, int TM, int TN, int EPI>
+// Choice measured on the pass's shapes: the 256 x 256 tile when it still yields enough
+// tiles (residual updates split K, so fewer suffice), else 256 x 128.
+GemmPlan gemm_plan(int epi, int M, int N, int K, int num_cus) {
+  if (M <= 64) return gemm_plan_cfg(epi, M, N, K, num_cus, 1);
+  const int tiles0 = ((M + 255) / 256) * ((N + 255) / 256);
+  const int need = epi == EPI_ADD_F32 ? num_cus / 4 : (num_cus * 3) / 4;
+  return gemm_plan_cfg(epi, M, N, K, num_cus, tiles0 >= need ? 0 : 2);
+}
+
+template <int WAVES_M, int WAVES_N, int TM, int TN, int EPI, int DEPTH>
 static hipError_t run(const GemmArgs& a, int grid, hipStream_t s) {
-  hipLaunchKernelGGL((k_gemm<WAVES_M, WAVES_N, TM, TN, EPI>), dim3(grid),
+  hipLaunchKernelGGL((k_gemm<WAVES_M, WAVES_N, TM, TN, EPI, DEPTH>), dim3(grid),
                      dim3(WAVES_M * WAVES_N * 64), 0, s, a);
   return hipGetLastError();
+}
+
+template <int EPI>
+static hipError_t run_cfg(int cfg, const GemmArgs& a, int grid, hipStream_t s) {
+  switch (cfg) {
+    case 0: return run<4, 4, 2, 2, EPI, 1>(a, grid, s);
+    case 1:
+      if constexpr (EPI == EPI_SWIGLU) return run<1, 2, 1, 2, EPI, 2>(a, grid, s);
+      else return run<1, 4, 1, 1, EPI, 2>(a, grid, s);
+    default: return run<4, 2, 2, 2, EPI, 1>(a, grid, s);
+  }
 }
 
 hipError_t launch_gemm(int epi, const GemmArgs& in, const GemmPlan& p, hipStream_t s) {
@@ -286,16 +341,10 @@ hipError_t launch_gemm(int epi, const GemmArgs& in, const GemmPlan& p, hipStream
   GemmArgs a = in;
   a.splits = p.splits;
   const int grid = p.tiles * p.splits;
-  const bool small = p.cfg == CFG_SMALL_M;
   switch (epi) {
-    case EPI_BF16:
-      return small ? run<1, 4, 1, 1, EPI_BF16>(a, grid, s) : run<2, 2, 4, 2, EPI_BF16>(a, grid, s);
-    case EPI_ADD_F32:
-      return small ? run<1, 4, 1, 1, EPI_ADD_F32>(a, grid, s)
-                   : run<2, 2, 4, 2, EPI_ADD_F32>(a, grid, s);
-    case EPI_SWIGLU:
-      return small ? run<1, 2, 1, 2, EPI_SWIGLU>(a, grid, s)
-                   : run<2, 2, 4, 2, EPI_SWIGLU>(a, grid, s);
+    case EPI_BF16: return run_cfg<EPI_BF16>(p.cfg, a, grid, s);
+    case EPI_ADD_F32: return run_cfg<EPI_ADD_F32>(p.cfg, a, grid, s);
+    case EPI_SWIGLU: return run_cfg<EPI_SWIGLU>(p.cfg, a, grid, s);
   }
   return hipErrorInvalidValue;
 }

@@ -55,7 +55,9 @@ struct GemmPlan {
 // Tile configuration and K split for one GEMM shape.  Split-K workspace never exceeds
 // gemm_ws_floats_bound(num_cus) floats and num_cus tickets.
 GemmPlan gemm_plan(int epi, int M, int N, int K, int num_cus);
-inline size_t gemm_ws_floats_bound(int num_cus) { return (size_t)2 * num_cus * 256 * 128; }
+GemmPlan gemm_plan_cfg(int epi, int M, int N, int K, int num_cus, int cfg);
+int gemm_num_cfgs();
+inline size_t gemm_ws_floats_bound(int num_cus) { return (size_t)2 * num_cus * 256 * 256; }
 hipError_t launch_gemm(int epi, const GemmArgs& a, const GemmPlan& p, hipStream_t s);
 
 // ---- attention ---------------------------------------------------------------------------

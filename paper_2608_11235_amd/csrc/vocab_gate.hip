@@ -7,8 +7,8 @@
 // is the lowest id among equal maxima, the mask id is skipped, and the confidence
 // is c = max softmax = 1 / sum_v exp(l_v - l_max) (Eq. 1).
 //
-// Phase 2, the last workgroup of each batch row to finish (a per-row ticket taken
-// after a device-scope fence) applies, on that row's active block:
+// Phase 2, the last workgroup of each batch row to finish (a per-row ticket taken after
+// its agent-coherent result stores completed) applies, on that row's active block:
 //   block step 0 -> previous top-1 and counters reset (persistence is per block);
 //   Eq. (2) counter update on unresolved positions;
 //   transfer rule: the k highest-confidence unresolved positions (ties -> lower position);
@@ -123,21 +123,23 @@ __global__ __launch_bounds__(256) void k_vocab_gate(VocabGateArgs a) {
   if (tid == 0) {
     TopState r{sm_m[0], sm_s[0], sm_a[0]};
     for (int w = 1; w < 4; ++w) r = merge(r, TopState{sm_m[w], sm_s[w], sm_a[w]});
-    a.top1[row] = r.arg;
-    a.conf[row] = 1.0f / r.s;
-    __threadfence();
-    const int old = atomicAdd(&a.tickets[b], 1);
+    // agent-coherent (sc1) stores instead of a release fence, which would write back the
+    // whole L2: once they complete (vmcnt 0) they are visible to the last workgroup
+    __hip_atomic_store(&a.top1[row], r.arg, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&a.conf[row], 1.0f / r.s, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __builtin_amdgcn_s_waitcnt(0);
+    const int old =
+        __hip_atomic_fetch_add(&a.tickets[b], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     is_last = (old == a.n_rows - 1);
   }
   __syncthreads();
   if (!is_last) return;
-  __threadfence();
 
   // ---- phase 2: decision rules for batch row b --------------------------------------
   const int BL = a.block_len;
   const int blk = a.block_idx[b];
   const int s = a.step_idx[b];
-  if (tid == 0) a.tickets[b] = 0;
+  if (tid == 0) __hip_atomic_store(&a.tickets[b], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   if (blk < 0 || s < 0) {  // malformed state: touch nothing outside the scored rows
     if (tid == 0) a.done[b] = 0;
     return;
@@ -159,8 +161,8 @@ __global__ __launch_bounds__(256) void k_vocab_gate(VocabGateArgs a) {
   if (act) {
     U = a.unresolved[gi];
     const int64_t ri = (int64_t)b * a.n_rows + (lo + tid - row0);
-    xh = a.top1[ri];
-    c = a.conf[ri];
+    xh = __hip_atomic_load(&a.top1[ri], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    c = __hip_atomic_load(&a.conf[ri], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     int prev = s == 0 ? -1 : a.prev_top1[gi];
     int mm = s == 0 ? 0 : a.persist[gi];
     if (U) {                                              // Eq. (2)

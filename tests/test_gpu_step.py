@@ -26,10 +26,11 @@ pytestmark = pytest.mark.gpu
 SPEC = si.TINY
 # With N(0, 0.02) weights every masked position sees the same input and near-uniform
 # attention, so block confidences differ by ~1e-3 in ln c: almost every transfer cut is
-# within the bf16 logit error and excluded.  The same shape drawn with std 0.2 spreads
-# confidences and margins, so most decisions are comparable; it is an extra parity model.
-SEPARATED = replace(si.TINY, name="tiny-std0.2", init_std=0.2, logit_scale=1.0)
-MODELS = [pytest.param(SPEC, 0.0, id="tiny"), pytest.param(SEPARATED, 0.5, id="tiny-std0.2")]
+# within the bf16 logit error and excluded.  The same shape drawn with std 0.07 (logits x2)
+# spreads confidences and margins while bf16 activation rounding stays under 1.4 % of the
+# largest logit, so over half of the decisions are comparable; it is an extra parity model.
+SEPARATED = replace(si.TINY, name="tiny-std0.07", init_std=0.07, logit_scale=2.0)
+MODELS = [pytest.param(SPEC, 0.0, id="tiny"), pytest.param(SEPARATED, 0.4, id="tiny-std0.07")]
 P, G, BLK, S = 32, 64, 32, 16
 L = P + G
 
