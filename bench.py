@@ -21,10 +21,28 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
+import hashlib
+
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 B, P, G, BLK, S = 1, 256, 256, 32, 32
 DELTA_P, M_REQ = 0.65, 1
+
+
+# HBM bytes per launch from rocprofv3 FETCH_SIZE (x2.0) + WRITE_SIZE (x1.0) runs, scaled by a
+# plain 1 GiB copy (profiles/gate_up_gemm_llada8b_gen256.md, profiles/vocab_gate_8x512x126464.md).
+# Valid only for the kernel source the counters were taken on.
+COUNTER_TRAFFIC = {
+    "gate_up": ("paper_2608_11235_amd/csrc/gemm.hip", "bfb20c85ff602a87", 247642726),
+    "vocab_gate": ("paper_2608_11235_amd/csrc/vocab_gate.hip", "ba73da83ca2a6a22", 1036616704),
+}
+
+
+def counter_traffic(name):
+    path, digest, nbytes = COUNTER_TRAFFIC[name]
+    with open(os.path.join(ROOT, path), "rb") as f:
+        now = hashlib.sha256(f.read()).hexdigest()[:16]
+    return nbytes if now == digest else None
 
 
 def pass_flops(spec, M, rows):
@@ -112,8 +130,28 @@ def vocab_gate_roofline(iters=20):
     nbytes = Bv * R * V * 2
     ach = nbytes / (ms * 1e-3) / 1e9
     return {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-            "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None, "us_per_launch": round(ms * 1e3, 2),
+            "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": counter_traffic("vocab_gate"),
+            "us_per_launch": round(ms * 1e3, 2),
             "workload": "bf16 logits [8, 512, 126464], k = 1"}
+
+
+def copy_calibration(nbytes=1 << 30, iters=5):
+    """A plain device-to-device copy of known size: reference for HBM byte counters."""
+    import torch
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(iters):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / iters
+    print(json.dumps({"copy_bytes_read": nbytes, "copy_bytes_written": nbytes, "iters": iters,
+                      "us_per_copy": round(ms * 1e3, 2),
+                      "GB_per_s_read_plus_write": round(2 * nbytes / (ms * 1e-3) / 1e9, 1)}),
+          flush=True)
 
 
 def main():
@@ -124,7 +162,18 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-vocab", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--only", choices=["all", "pass", "vocab", "copy"], default="all",
+                    help="run one leg only (profiling runs): the timed passes, the vocab/gate "
+                         "kernel, or a plain 1 GiB device copy that calibrates byte counters")
     args = ap.parse_args()
+    if args.only == "copy":
+        copy_calibration()
+        return
+    if args.only == "vocab":
+        print(json.dumps({"vocab_gate_roofline": vocab_gate_roofline()}), flush=True)
+        return
+    if args.only == "pass":
+        args.no_decode = args.no_vocab = args.no_cpu_baseline = True
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (batch rows "
               "decode independently, so more GPUs shard rows with no collective)", file=sys.stderr)
@@ -190,7 +239,8 @@ def main():
         "pass_mfma_frac": round(fl_pass / (ms_per_step * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
         "roofline": {"bound": "mfma", "achieved": round(gu_tflops, 1), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(gu_tflops / PEAK_BF16_TFLOPS, 4),
-                     "traffic": None, "kernel": "gate/up SwiGLU GEMM (M 512, N 24576, K 4096)",
+                     "traffic": counter_traffic("gate_up"),
+                     "kernel": "gate/up SwiGLU GEMM (M 512, N 24576, K 4096)",
                      "us_per_launch": round(gu_avg_ms * 1e3, 2), "launches": gu_launches},
         "model_create_s": round(t_create, 2),
     }

@@ -3,7 +3,8 @@
 // Inputs: q [B, H, Ls, hd], k [B, Hkv, Ls, hd] (RoPE applied), vt [B, Hkv, hd, Ls]
 // (v transposed), rows >= L zero.  Output: o [B * L, H * hd] bf16.
 // One workgroup = 64 queries of one head (4 wavefronts x 16 queries); key tiles of 64
-// are staged in LDS.  Everything is computed transposed with
+// are staged in LDS, double buffered: the next tile's loads are in flight in registers
+// while the current tile is multiplied out of LDS (one barrier per tile).  Everything is computed transposed with
 // v_mfma_f32_16x16x32_bf16 so that a query's softmax statistics never leave its lanes:
 //   S^T = K Q^T   (A = K tile from LDS, B = Q^T held in registers)
 //   O^T = V^T P^T (A = V^T tile from LDS, B = P^T straight from the S^T registers)
@@ -24,8 +25,9 @@ __global__ __launch_bounds__(256) void k_attention(const uint16_t* __restrict__ 
   constexpr int KT = 64;          // keys per tile
   constexpr int LDKS = HD + 8;    // padded LDS rows
   constexpr int LDVS = KT + 8;
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[KT * LDKS];
-  __shared__ __attribute__((aligned(16))) uint16_t Vs[HD * LDVS];
+  constexpr int CK = KT * HD / 8 / 256;  // 16-byte chunks per thread per tile (K and V^T each)
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][KT * LDKS];
+  __shared__ __attribute__((aligned(16))) uint16_t Vs[2][HD * LDVS];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int bh = blockIdx.y, b = bh / H, h = bh % H, kvh = h / (H / Hkv);
@@ -46,21 +48,36 @@ __global__ __launch_bounds__(256) void k_attention(const uint16_t* __restrict__ 
   for (int d = 0; d < HD / 16; ++d) o[d] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_part = 0.f;
 
+  // K tile [64 keys][HD] and V^T tile [HD][64 keys]: chunk c of this thread
+  u32x4_t rk[CK], rv[CK];
+  auto fetch = [&](int key0) {
+#pragma unroll
+    for (int i = 0; i < CK; ++i) {
+      const int c = tid + i * 256;
+      const int kr = c / (HD / 8), kc = (c % (HD / 8)) * 8;
+      rk[i] = *reinterpret_cast<const u32x4_t*>(kh + (int64_t)(key0 + kr) * HD + kc);
+      const int vr = c / (KT / 8), vc = (c % (KT / 8)) * 8;
+      rv[i] = *reinterpret_cast<const u32x4_t*>(vh + (int64_t)vr * Ls + key0 + vc);
+    }
+  };
+  auto stash = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < CK; ++i) {
+      const int c = tid + i * 256;
+      const int kr = c / (HD / 8), kc = (c % (HD / 8)) * 8;
+      *reinterpret_cast<u32x4_t*>(&Ks[buf][kr * LDKS + kc]) = rk[i];
+      const int vr = c / (KT / 8), vc = (c % (KT / 8)) * 8;
+      *reinterpret_cast<u32x4_t*>(&Vs[buf][vr * LDVS + vc]) = rv[i];
+    }
+  };
+
   const int n_tiles = (L + KT - 1) / KT;
+  fetch(0);
+  stash(0);
+  __syncthreads();
   for (int kt = 0; kt < n_tiles; ++kt) {
-    const int key0 = kt * KT;
-    // stage K [64][HD] and V^T [HD][64]
-    for (int c = tid; c < KT * HD / 8; c += 256) {
-      const int r = c / (HD / 8), cc = (c % (HD / 8)) * 8;
-      *reinterpret_cast<u32x4_t*>(&Ks[r * LDKS + cc]) =
-          *reinterpret_cast<const u32x4_t*>(kh + (int64_t)(key0 + r) * HD + cc);
-    }
-    for (int c = tid; c < HD * KT / 8; c += 256) {
-      const int r = c / (KT / 8), cc = (c % (KT / 8)) * 8;
-      *reinterpret_cast<u32x4_t*>(&Vs[r * LDVS + cc]) =
-          *reinterpret_cast<const u32x4_t*>(vh + (int64_t)r * Ls + key0 + cc);
-    }
-    __syncthreads();
+    const int buf = kt & 1, key0 = kt * KT;
+    if (kt + 1 < n_tiles) fetch(key0 + KT);  // next tile in flight during this one
 
     f32x4_t st[4];
 #pragma unroll
@@ -69,7 +86,7 @@ __global__ __launch_bounds__(256) void k_attention(const uint16_t* __restrict__ 
 #pragma unroll
       for (int kk = 0; kk < HD / 32; ++kk) {
         const bf16x8_t a = as_bf16x8(
-            *reinterpret_cast<const u32x4_t*>(&Ks[(kb * 16 + r16) * LDKS + kk * 32 + g * 8]));
+            *reinterpret_cast<const u32x4_t*>(&Ks[buf][(kb * 16 + r16) * LDKS + kk * 32 + g * 8]));
         st[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[kk], st[kb], 0, 0, 0);
       }
     }
@@ -109,13 +126,14 @@ __global__ __launch_bounds__(256) void k_attention(const uint16_t* __restrict__ 
       const bf16x8_t bfrag = as_bf16x8(pb);
 #pragma unroll
       for (int d = 0; d < HD / 16; ++d) {
-        const uint16_t* vrow = &Vs[(d * 16 + r16) * LDVS + ks * 32 + g * 4];
+        const uint16_t* vrow = &Vs[buf][(d * 16 + r16) * LDVS + ks * 32 + g * 4];
         const u32x2_t lo = *reinterpret_cast<const u32x2_t*>(vrow);
         const u32x2_t hi = *reinterpret_cast<const u32x2_t*>(vrow + 16);
         const u32x4_t av = u32x4_t{lo.x, lo.y, hi.x, hi.y};
         o[d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(av), bfrag, o[d], 0, 0, 0);
       }
     }
+    if (kt + 1 < n_tiles) stash(buf ^ 1);
     __syncthreads();
   }
 

@@ -21,6 +21,8 @@
 //             EPI_SWIGLU  weights interleave gate/up rows in groups of 32, so a
 //                         wavefront's two 32-column blocks hold gate and up of the
 //                         same outputs: C = bf16(silu(g) * u), ldc over ffn columns.
+//             EPI_QKV_ROPE  bias, rotate-half RoPE on q and k, head-major q/k and
+//                         transposed v written straight from the accumulators.
 // Requirements: K % (64 * splits) == 0; M, N arbitrary (tails clamped on load, masked
 // on store).
 #include "common.hpp"
@@ -247,6 +249,42 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void k_gemm(GemmArgs g) {
           }
         }
     }
+  } else if constexpr (EPI == EPI_QKV_ROPE) {
+    // q/k columns are pair-interleaved within a head, so the rotate-half partner of
+    // column c is column c ^ 1, held by lane ^ 1 for the same rows
+    const QkvOut& o = g.qkv;
+    const int hd = o.head_dim, half = hd / 2;
+    const int hq = o.n_heads * hd, hkv = o.n_kv_heads * hd;
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int col = n0 + wn * TN * 32 + j * 32 + col_l;
+      const bool in = col < g.N;
+      const float bias = (in && g.bias) ? g.bias[col] : 0.f;
+      const int sec = col < hq ? 0 : (col < hq + hkv ? 1 : 2);
+      const int cc = col - (sec == 0 ? 0 : (sec == 1 ? hq : hq + hkv));
+      const int head = cc / hd, pd = cc % hd;
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const float x = acc[i][j][e] + bias;
+          const float partner = __shfl_xor(x, 1, 64);
+          const int row = m0 + wm * TM * 32 + i * 32 + 8 * (e >> 2) + row_q + (e & 3);
+          if (!in || row >= g.M) continue;
+          const int b = row / o.L, pos = row - b * o.L;
+          if (sec < 2) {
+            const int ii = pd >> 1;
+            const float c = o.cos_t[pos * half + ii], sn = o.sin_t[pos * half + ii];
+            const float r = (pd & 1) ? x * c + partner * sn : x * c - partner * sn;
+            uint16_t* dst = sec == 0 ? o.q + ((int64_t)(b * o.n_heads + head) * o.Ls + pos) * hd
+                                     : o.k + ((int64_t)(b * o.n_kv_heads + head) * o.Ls + pos) * hd;
+            dst[pd] = (uint16_t)f32_to_bf16_bits(r);
+          } else {
+            o.vt[((int64_t)(b * o.n_kv_heads + head) * hd + pd) * o.Ls + pos] =
+                (uint16_t)f32_to_bf16_bits(x);
+          }
+        }
+    }
   } else {
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
@@ -345,6 +383,7 @@ hipError_t launch_gemm(int epi, const GemmArgs& in, const GemmPlan& p, hipStream
     case EPI_BF16: return run_cfg<EPI_BF16>(p.cfg, a, grid, s);
     case EPI_ADD_F32: return run_cfg<EPI_ADD_F32>(p.cfg, a, grid, s);
     case EPI_SWIGLU: return run_cfg<EPI_SWIGLU>(p.cfg, a, grid, s);
+    case EPI_QKV_ROPE: return run_cfg<EPI_QKV_ROPE>(p.cfg, a, grid, s);
   }
   return hipErrorInvalidValue;
 }

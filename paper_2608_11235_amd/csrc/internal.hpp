@@ -8,12 +8,16 @@ namespace cora {
 // ---- weight init (K10) ------------------------------------------------------------------
 // Physical row of logical row r: 0 identity (+row_offset), 1 gate half and 2 up half of
 // the 32-row interleaved gate/up matrix.
-enum RowMap { ROW_IDENTITY = 0, ROW_GATE = 1, ROW_UP = 2 };
+// 3: rows of q or k heads stored pair-interleaved within each head of hd rows (logical
+// j < hd/2 at 2j, logical j + hd/2 at 2j + 1), after row_offset.
+enum RowMap { ROW_IDENTITY = 0, ROW_GATE = 1, ROW_UP = 2, ROW_ROPE_PAIR = 3 };
 hipError_t launch_init_bf16(uint16_t* dst, uint64_t seed, uint64_t tensor_id, int64_t rows,
                             int64_t cols, int64_t ld, int row_map, int64_t row_offset, double std_dev,
-                            hipStream_t s);
+                            int head_dim, hipStream_t s);
 hipError_t launch_init_f32(float* dst, uint64_t seed, uint64_t tensor_id, int64_t n, double std_dev,
-                           hipStream_t s);
+                           int pair_head_dim, hipStream_t s);
+// physical position of logical index j inside a head of hd pair-interleaved rows
+__host__ __device__ inline int rope_pair_pos(int j, int hd) { return j < hd / 2 ? 2 * j : 2 * (j - hd / 2) + 1; }
 hipError_t launch_fill_f32(float* dst, float v, int64_t n, hipStream_t s);
 
 // ---- elementwise ------------------------------------------------------------------------
@@ -27,16 +31,22 @@ struct RowSel {
 };
 hipError_t launch_rmsnorm(const float* h, const float* w, uint16_t* out, int rows, int d,
                           float eps, RowSel sel, hipStream_t s);
-hipError_t launch_rope_split(const uint16_t* qkv, uint16_t* q, uint16_t* k, uint16_t* vt,
-                             const float* cos_t, const float* sin_t, int B, int L, int Ls, int H,
-                             int Hkv, int hd, hipStream_t s);
 hipError_t launch_state_init(const int32_t* prompt, int B, int P, int G, int mask_id,
                              int32_t* tokens, uint8_t* unresolved, int32_t* prev, int32_t* persist,
                              int32_t* block_idx, int32_t* step_idx, int32_t* passes, int n_blocks,
                              hipStream_t s);
 
 // ---- GEMM: C[M, N] = A[M, K] . W[N, K]^T, bf16 in, fp32 accumulate ---------------------
-enum GemmEpi { EPI_BF16 = 0, EPI_ADD_F32 = 1, EPI_SWIGLU = 2 };
+enum GemmEpi { EPI_BF16 = 0, EPI_ADD_F32 = 1, EPI_SWIGLU = 2, EPI_QKV_ROPE = 3 };
+// EPI_QKV_ROPE: columns [0, H*hd) are q heads, then Hkv*hd k heads, then Hkv*hd v heads;
+// q and k weight rows are pair-interleaved per head (ROW_ROPE_PAIR).  Adds the bias,
+// rotates q and k (rotate-half RoPE at position row % L), and writes q [B, H, Ls, hd],
+// k [B, Hkv, Ls, hd] in the interleaved dim order and v transposed vt [B, Hkv, hd, Ls].
+struct QkvOut {
+  uint16_t *q, *k, *vt;
+  const float *cos_t, *sin_t;  // [Ls, hd/2]
+  int L, Ls, n_heads, n_kv_heads, head_dim;
+};
 struct GemmArgs {
   const uint16_t* A; int64_t lda;
   const uint16_t* W; int64_t ldw;
@@ -47,6 +57,7 @@ struct GemmArgs {
   int splits;          // set by launch_gemm from the plan
   float* ws;           // split-K partials (GemmPlan::ws_floats floats)
   int32_t* counters;   // split-K tickets, one per tile, zero on entry and exit
+  QkvOut qkv;          // EPI_QKV_ROPE destinations
 };
 struct GemmPlan {
   int cfg, tiles, splits;

@@ -1,5 +1,4 @@
-// Weight init (counter-based generator), embedding gather, RMSNorm, RoPE + head
-// split, and decode-state init.
+// Weight init (counter-based generator), embedding gather, RMSNorm and decode-state init.
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -29,11 +28,12 @@ __device__ __forceinline__ float normal_from_counter(uint64_t key, uint64_t ctr,
 
 __global__ void k_init_bf16(uint16_t* __restrict__ dst, uint64_t key, uint64_t base, int64_t rows,
                             int64_t cols, int64_t ld, int row_map, int64_t row_offset,
-                            double std_dev) {
+                            double std_dev, int hd) {
   for (int64_t r = blockIdx.x; r < rows; r += gridDim.x) {
     int64_t pr;
     if (row_map == ROW_GATE) pr = (r >> 5) * 64 + (r & 31);
     else if (row_map == ROW_UP) pr = (r >> 5) * 64 + 32 + (r & 31);
+    else if (row_map == ROW_ROPE_PAIR) pr = row_offset + (r / hd) * hd + rope_pair_pos((int)(r % hd), hd);
     else pr = row_offset + r;
     uint16_t* out = dst + pr * ld;
     for (int64_t c = threadIdx.x; c < cols; c += blockDim.x) {
@@ -45,11 +45,12 @@ __global__ void k_init_bf16(uint16_t* __restrict__ dst, uint64_t key, uint64_t b
 
 // bias vectors: drawn like any tensor, rounded to bf16, stored as fp32
 __global__ void k_init_f32(float* __restrict__ dst, uint64_t key, uint64_t base, int64_t n,
-                           double std_dev) {
+                           double std_dev, int pair_hd) {
   for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < n;
        e += (int64_t)gridDim.x * blockDim.x) {
     const float v = normal_from_counter(key, base | (uint64_t)e, std_dev);
-    dst[e] = bf16_bits_to_f32(f32_to_bf16_bits(v));
+    const int64_t pe = pair_hd > 0 ? (e / pair_hd) * pair_hd + rope_pair_pos((int)(e % pair_hd), pair_hd) : e;
+    dst[pe] = bf16_bits_to_f32(f32_to_bf16_bits(v));
   }
 }
 
@@ -70,18 +71,18 @@ static uint64_t host_mix64(uint64_t z) {
 
 hipError_t launch_init_bf16(uint16_t* dst, uint64_t seed, uint64_t tensor_id, int64_t rows,
                             int64_t cols, int64_t ld, int row_map, int64_t row_offset, double std_dev,
-                            hipStream_t s) {
+                            int head_dim, hipStream_t s) {
   const int grid = (int)(rows < 16384 ? rows : 16384);
   hipLaunchKernelGGL(k_init_bf16, dim3(grid), dim3(256), 0, s, dst, host_mix64(seed),
-                     tensor_id << 40, rows, cols, ld, row_map, row_offset, std_dev);
+                     tensor_id << 40, rows, cols, ld, row_map, row_offset, std_dev, head_dim);
   return hipGetLastError();
 }
 
 hipError_t launch_init_f32(float* dst, uint64_t seed, uint64_t tensor_id, int64_t n,
-                           double std_dev, hipStream_t s) {
+                           double std_dev, int pair_head_dim, hipStream_t s) {
   const int grid = (int)((n + 255) / 256 < 4096 ? (n + 255) / 256 : 4096);
   hipLaunchKernelGGL(k_init_f32, dim3(grid), dim3(256), 0, s, dst, host_mix64(seed),
-                     tensor_id << 40, n, std_dev);
+                     tensor_id << 40, n, std_dev, pair_head_dim);
   return hipGetLastError();
 }
 
@@ -161,60 +162,6 @@ hipError_t launch_rmsnorm(const float* h, const float* w, uint16_t* out, int row
                           float eps, RowSel sel, hipStream_t s) {
   if (rows == 0) return hipSuccess;
   hipLaunchKernelGGL(k_rmsnorm, dim3(rows), dim3(256), 0, s, h, w, out, d, eps, sel);
-  return hipGetLastError();
-}
-
-// ---- RoPE (rotate-half) on q and k, head-major split, v transposed ----------------------
-// qkv [B*L, (H + 2 Hkv) * hd] -> q [B, H, Ls, hd], k [B, Hkv, Ls, hd], vt [B, Hkv, hd, Ls];
-// positions L..Ls-1 are written as zeros.  One block = 64 positions of one head.
-__global__ __launch_bounds__(256) void k_rope_split(const uint16_t* __restrict__ qkv,
-                                                    uint16_t* __restrict__ q,
-                                                    uint16_t* __restrict__ k,
-                                                    uint16_t* __restrict__ vt,
-                                                    const float* __restrict__ cos_t,
-                                                    const float* __restrict__ sin_t, int L,
-                                                    int Ls, int H, int Hkv, int hd) {
-  const int p0 = blockIdx.x * 64, b = blockIdx.y, hh = blockIdx.z;
-  const int ldq = (H + 2 * Hkv) * hd;
-  const int half = hd / 2;
-  if (hh < H + Hkv) {
-    uint16_t* dst;
-    if (hh < H) dst = q + ((int64_t)(b * H + hh) * Ls) * hd;
-    else dst = k + ((int64_t)(b * Hkv + (hh - H)) * Ls) * hd;
-    for (int e = threadIdx.x; e < 64 * half; e += 256) {
-      const int p = e / half, j = e % half, pos = p0 + p;
-      float o1 = 0.f, o2 = 0.f;
-      if (pos < L) {
-        const uint16_t* src = qkv + ((int64_t)b * L + pos) * ldq + hh * hd;
-        const float x1 = bf16_bits_to_f32(src[j]), x2 = bf16_bits_to_f32(src[j + half]);
-        const float c = cos_t[pos * half + j], sn = sin_t[pos * half + j];
-        o1 = x1 * c - x2 * sn;
-        o2 = x2 * c + x1 * sn;
-      }
-      dst[(int64_t)pos * hd + j] = (uint16_t)f32_to_bf16_bits(o1);
-      dst[(int64_t)pos * hd + j + half] = (uint16_t)f32_to_bf16_bits(o2);
-    }
-  } else {
-    __shared__ uint16_t tile[64][128 + 2];
-    const int kvh = hh - H - Hkv;
-    for (int e = threadIdx.x; e < 64 * hd; e += 256) {
-      const int p = e / hd, c = e % hd, pos = p0 + p;
-      tile[p][c] = pos < L ? qkv[((int64_t)b * L + pos) * ldq + hh * hd + c] : (uint16_t)0;
-    }
-    __syncthreads();
-    uint16_t* dst = vt + ((int64_t)(b * Hkv + kvh) * hd) * Ls;
-    for (int e = threadIdx.x; e < 64 * hd; e += 256) {
-      const int c = e / 64, p = e % 64;
-      dst[(int64_t)c * Ls + p0 + p] = tile[p][c];
-    }
-  }
-}
-
-hipError_t launch_rope_split(const uint16_t* qkv, uint16_t* q, uint16_t* k, uint16_t* vt,
-                             const float* cos_t, const float* sin_t, int B, int L, int Ls, int H,
-                             int Hkv, int hd, hipStream_t s) {
-  hipLaunchKernelGGL(k_rope_split, dim3(Ls / 64, B, H + 2 * Hkv), dim3(256), 0, s, qkv, q, k, vt,
-                     cos_t, sin_t, L, Ls, H, Hkv, hd);
   return hipGetLastError();
 }
 

@@ -63,7 +63,7 @@ struct cora_model {
 
   // workspace
   float* h = nullptr;
-  uint16_t *a = nullptr, *qkv = nullptr, *q = nullptr, *k = nullptr, *vt = nullptr;
+  uint16_t *a = nullptr, *q = nullptr, *k = nullptr, *vt = nullptr;
   uint16_t *attn = nullptr, *u = nullptr, *logits = nullptr;
   float *rope_cos = nullptr, *rope_sin = nullptr;
   int32_t* tickets = nullptr;
@@ -159,7 +159,7 @@ extern "C" cora_status cora_model_create(const cora_model_cfg* cfg, uint64_t see
   }
   const size_t skw = gemm_ws_floats_bound(m->num_cus);
   size_t wsb = align_up(skw * 4) + align_up((size_t)m->num_cus * 4) + align_up(M * d * 4) + align_up(M * (size_t)(d > m->hq ? d : m->hq) * 2) +
-               align_up(M * m->qkv_n * 2) + align_up(Ms * m->hq * 2) + 2 * align_up(Ms * m->hkv * 2) +
+               align_up(Ms * m->hq * 2) + 2 * align_up(Ms * m->hkv * 2) +
                align_up(M * m->hq * 2) + align_up(M * m->f_pad * 2) + align_up(rows * V * 2) +
                2 * align_up((size_t)m->max_seq_pad * (hd / 2) * 4) + align_up(max_batch * 4) +
                // decode state
@@ -197,7 +197,6 @@ extern "C" cora_status cora_model_create(const cora_model_cfg* cfg, uint64_t see
   m->splitk_cnt = a.take<int32_t>(m->num_cus);
   m->h = a.take<float>(M * d);
   m->a = a.take<uint16_t>(M * (d > m->hq ? d : m->hq));
-  m->qkv = a.take<uint16_t>(M * m->qkv_n);
   m->q = a.take<uint16_t>(Ms * m->hq);
   m->k = a.take<uint16_t>(Ms * m->hkv);
   m->vt = a.take<uint16_t>(Ms * m->hkv);
@@ -230,25 +229,27 @@ extern "C" cora_status cora_model_create(const cora_model_cfg* cfg, uint64_t see
     HIP_TRY(hipMemsetAsync(m->tickets, 0, max_batch * sizeof(int32_t), s));
     HIP_TRY(hipMemsetAsync(m->splitk_cnt, 0, m->num_cus * sizeof(int32_t), s));
     const double sd = cfg->init_std;
-    HIP_TRY(launch_init_bf16(m->embed, seed, 1, V, d, d, ROW_IDENTITY, 0, sd, s));
-    HIP_TRY(launch_init_bf16(m->lm_head, seed, 2, V, d, d, ROW_IDENTITY, 0, sd, s));
+    HIP_TRY(hipMemsetAsync(m->ws_mem, 0, wsb, s));  // finite zeros in every padding region
+    HIP_TRY(launch_init_bf16(m->embed, seed, 1, V, d, d, ROW_IDENTITY, 0, sd, hd, s));
+    HIP_TRY(launch_init_bf16(m->lm_head, seed, 2, V, d, d, ROW_IDENTITY, 0, sd, hd, s));
     HIP_TRY(launch_fill_f32(m->ones, 1.0f, d, s));
     for (int l = 0; l < (int)L_; ++l) {
       const auto& ly = m->layers[l];
       const uint64_t t0 = 100 + 16 * (uint64_t)l;
-      HIP_TRY(launch_init_bf16(ly.wqkv, seed, t0 + 0, m->hq, d, d, ROW_IDENTITY, 0, sd, s));
-      HIP_TRY(launch_init_bf16(ly.wqkv, seed, t0 + 1, m->hkv, d, d, ROW_IDENTITY, m->hq, sd, s));
-      HIP_TRY(launch_init_bf16(ly.wqkv, seed, t0 + 2, m->hkv, d, d, ROW_IDENTITY, m->hq + m->hkv,
-                               sd, s));
-      HIP_TRY(launch_init_bf16(ly.wo, seed, t0 + 3, d, m->hq, m->hq, ROW_IDENTITY, 0, sd, s));
-      HIP_TRY(launch_init_bf16(ly.wgu, seed, t0 + 4, cfg->ffn_dim, d, d, ROW_GATE, 0, sd, s));
-      HIP_TRY(launch_init_bf16(ly.wgu, seed, t0 + 5, cfg->ffn_dim, d, d, ROW_UP, 0, sd, s));
-      HIP_TRY(launch_init_bf16(ly.wd, seed, t0 + 6, d, cfg->ffn_dim, m->f_pad, ROW_IDENTITY, 0, sd,
+      HIP_TRY(launch_init_bf16(ly.wqkv, seed, t0 + 0, m->hq, d, d, ROW_ROPE_PAIR, 0, sd, hd, s));
+      HIP_TRY(launch_init_bf16(ly.wqkv, seed, t0 + 1, m->hkv, d, d, ROW_ROPE_PAIR, m->hq, sd, hd,
                                s));
+      HIP_TRY(launch_init_bf16(ly.wqkv, seed, t0 + 2, m->hkv, d, d, ROW_IDENTITY, m->hq + m->hkv,
+                               sd, hd, s));
+      HIP_TRY(launch_init_bf16(ly.wo, seed, t0 + 3, d, m->hq, m->hq, ROW_IDENTITY, 0, sd, hd, s));
+      HIP_TRY(launch_init_bf16(ly.wgu, seed, t0 + 4, cfg->ffn_dim, d, d, ROW_GATE, 0, sd, hd, s));
+      HIP_TRY(launch_init_bf16(ly.wgu, seed, t0 + 5, cfg->ffn_dim, d, d, ROW_UP, 0, sd, hd, s));
+      HIP_TRY(launch_init_bf16(ly.wd, seed, t0 + 6, d, cfg->ffn_dim, m->f_pad, ROW_IDENTITY, 0, sd,
+                               hd, s));
       if (cfg->qkv_bias) {
-        HIP_TRY(launch_init_f32(ly.bqkv, seed, t0 + 7, m->hq, sd, s));
-        HIP_TRY(launch_init_f32(ly.bqkv + m->hq, seed, t0 + 8, m->hkv, sd, s));
-        HIP_TRY(launch_init_f32(ly.bqkv + m->hq + m->hkv, seed, t0 + 9, m->hkv, sd, s));
+        HIP_TRY(launch_init_f32(ly.bqkv, seed, t0 + 7, m->hq, sd, hd, s));
+        HIP_TRY(launch_init_f32(ly.bqkv + m->hq, seed, t0 + 8, m->hkv, sd, hd, s));
+        HIP_TRY(launch_init_f32(ly.bqkv + m->hq + m->hkv, seed, t0 + 9, m->hkv, sd, 0, s));
       }
     }
     // RoPE tables in fp64, stored fp32: angle = pos * theta^(-2j/hd)
@@ -343,10 +344,10 @@ static cora_status run_layers(cora_model* m, const int32_t* tokens, int B, int L
   const RowSel all{0, L, 0, 0, 0, 0, 0, nullptr};
   for (const auto& ly : m->layers) {
     HIP_TRY(launch_rmsnorm(m->h, m->ones, m->a, M, d, c.rms_eps, all, s));
-    GemmArgs g{m->a, d, ly.wqkv, d, M, m->qkv_n, d, m->qkv, m->qkv_n, ly.bqkv, 1.0f};
-    if (cora_status st = gemm(m, EPI_BF16, g, s)) return st;
-    HIP_TRY(launch_rope_split(m->qkv, m->q, m->k, m->vt, m->rope_cos, m->rope_sin, B, L, Ls,
-                              c.n_heads, c.n_kv_heads, c.head_dim, s));
+    GemmArgs g{m->a, d, ly.wqkv, d, M, m->qkv_n, d, nullptr, 0, ly.bqkv, 1.0f};
+    g.qkv = QkvOut{m->q, m->k, m->vt, m->rope_cos, m->rope_sin, L, Ls, c.n_heads, c.n_kv_heads,
+                   c.head_dim};
+    if (cora_status st = gemm(m, EPI_QKV_ROPE, g, s)) return st;
     HIP_TRY(launch_attention(m->q, m->k, m->vt, m->attn, B, L, Ls, c.n_heads, c.n_kv_heads,
                              c.head_dim, s));
     g = GemmArgs{m->attn, m->hq, ly.wo, m->hq, M, d, m->hq, m->h, d, nullptr, 1.0f};
@@ -555,7 +556,17 @@ extern "C" cora_status cora_model_copy_tensor(cora_model* m, int32_t tensor_id, 
       const int rows = j == 0 ? m->hq : m->hkv;
       const int off = j == 0 ? 0 : (j == 1 ? m->hq : m->hq + m->hkv);
       if (cora_status e = want((size_t)rows * d)) return e;
-      HIP_TRY(hipMemcpy(h_dst, ly.wqkv + (size_t)off * d, bytes, hipMemcpyDeviceToHost));
+      if (j == 2) {
+        HIP_TRY(hipMemcpy(h_dst, ly.wqkv + (size_t)off * d, bytes, hipMemcpyDeviceToHost));
+        return CORA_OK;
+      }
+      std::vector<uint16_t> tmp((size_t)rows * d);  // undo the per-head pair interleave
+      HIP_TRY(hipMemcpy(tmp.data(), ly.wqkv + (size_t)off * d, bytes, hipMemcpyDeviceToHost));
+      const int hd = c.head_dim;
+      for (int r = 0; r < rows; ++r) {
+        const size_t pr = (size_t)(r / hd) * hd + rope_pair_pos(r % hd, hd);
+        memcpy(out + (size_t)r * d, tmp.data() + pr * d, (size_t)d * 2);
+      }
       return CORA_OK;
     }
     case 3:
@@ -585,9 +596,11 @@ extern "C" cora_status cora_model_copy_tensor(cora_model* m, int32_t tensor_id, 
       if (cora_status e = want((size_t)n)) return e;
       std::vector<float> tmp(n);
       HIP_TRY(hipMemcpy(tmp.data(), ly.bqkv + off, (size_t)n * 4, hipMemcpyDeviceToHost));
+      const int hd = c.head_dim;
       for (int i = 0; i < n; ++i) {
+        const int pi = j == 9 ? i : (i / hd) * hd + rope_pair_pos(i % hd, hd);
         uint32_t u;
-        memcpy(&u, &tmp[i], 4);
+        memcpy(&u, &tmp[pi], 4);
         out[i] = (uint16_t)(u >> 16);
       }
       return CORA_OK;
