@@ -34,22 +34,27 @@ constexpr int BK = 64;
 constexpr int LDK = BK + 8;  // padded LDS row, in bf16 elements
 
 // n 16-byte loads at byte offset voff + i * step (step uniform) through a buffer resource
-template <int N>
+// n 16-byte loads at byte offset voff + i * step (step uniform) through a buffer resource;
+// when the chunks do not divide evenly, the last one exists only for threads with
+// tid + (N-1) * NT < total.
+template <int N, bool EXACT>
 __device__ __forceinline__ void buf_load(u32x4_t (&r)[N], __amdgpu_buffer_rsrc_t rs, int voff,
-                                         int step) {
+                                         int step, bool last_ok) {
 #pragma unroll
   for (int i = 0; i < N; ++i)
-    r[i] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, voff, i * step, 0));
+    if (EXACT || i + 1 < N || last_ok)
+      r[i] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, voff, i * step, 0));
 }
 
 template <int WAVES_M, int WAVES_N, int TM, int TN, int EPI, int DEPTH>
 __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void k_gemm(GemmArgs g) {
   constexpr int NT = WAVES_M * WAVES_N * 64;
   constexpr int BM = WAVES_M * TM * 32, BN = WAVES_N * TN * 32;
-  constexpr int CA = BM * BK / 8 / NT;  // 16-byte chunks per thread per slice
-  constexpr int CB = BN * BK / 8 / NT;
+  constexpr int CA = (BM * BK / 8 + NT - 1) / NT;  // 16-byte chunks per thread per slice
+  constexpr int CB = (BN * BK / 8 + NT - 1) / NT;
+  constexpr bool A_EXACT = CA * NT * 8 == BM * BK, B_EXACT = CB * NT * 8 == BN * BK;
   constexpr int NACC = TM * TN * 16;    // accumulators per thread
-  static_assert(CA * NT * 8 == BM * BK && CB * NT * 8 == BN * BK, "tile/thread mismatch");
+  static_assert(NT % 8 == 0, "threads must cover whole 64-element rows");
   static_assert(EPI != EPI_SWIGLU || TN % 2 == 0, "SwiGLU epilogue pairs 32-column blocks");
 
   __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * LDK];
@@ -82,6 +87,8 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void k_gemm(GemmArgs g) {
   const int b_step = (NT / 8) * (int)g.ldw * 2;
   const int lds_off = c_r * LDK + c_k;
   constexpr int LDS_STEP = (NT / 8) * LDK;
+  const bool a_last = tid + (CA - 1) * NT < BM * BK / 8;
+  const bool b_last = tid + (CB - 1) * NT < BN * BK / 8;
 
   f32x16_t acc[TM][TN];
 #pragma unroll
@@ -93,18 +100,20 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void k_gemm(GemmArgs g) {
 
   u32x4_t ra0[CA], rb0[CB];
   [[maybe_unused]] u32x4_t ra1[CA], rb1[CB];
-#define GEMM_FETCH(ra, rb, kt)                                   \
-  do {                                                           \
-    buf_load<CA>(ra, a_rs, a_off + (kt) * BK * 2, a_step);       \
-    buf_load<CB>(rb, b_rs, b_off + (kt) * BK * 2, b_step);       \
+#define GEMM_FETCH(ra, rb, kt)                                            \
+  do {                                                                    \
+    buf_load<CA, A_EXACT>(ra, a_rs, a_off + (kt) * BK * 2, a_step, a_last); \
+    buf_load<CB, B_EXACT>(rb, b_rs, b_off + (kt) * BK * 2, b_step, b_last); \
   } while (0)
   auto stash = [&](int buf, const u32x4_t(&ra)[CA], const u32x4_t(&rb)[CB]) {
 #pragma unroll
     for (int i = 0; i < CA; ++i)
-      *reinterpret_cast<u32x4_t*>(&As[buf][lds_off + i * LDS_STEP]) = ra[i];
+      if (A_EXACT || i + 1 < CA || a_last)
+        *reinterpret_cast<u32x4_t*>(&As[buf][lds_off + i * LDS_STEP]) = ra[i];
 #pragma unroll
     for (int i = 0; i < CB; ++i)
-      *reinterpret_cast<u32x4_t*>(&Bs[buf][lds_off + i * LDS_STEP]) = rb[i];
+      if (B_EXACT || i + 1 < CB || b_last)
+        *reinterpret_cast<u32x4_t*>(&Bs[buf][lds_off + i * LDS_STEP]) = rb[i];
   };
 
   // fragment read offsets: lane holds row (lane % 32), k half (lane / 32) * 8
@@ -251,7 +260,9 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void k_gemm(GemmArgs g) {
     }
   } else if constexpr (EPI == EPI_QKV_ROPE) {
     // q/k columns are pair-interleaved within a head, so the rotate-half partner of
-    // column c is column c ^ 1, held by lane ^ 1 for the same rows
+    // column c is column c ^ 1, held by lane ^ 1 for the same rows.  A lane's rows come in
+    // groups of 4 consecutive rows: one division per group, and v (stored transposed) is
+    // written as 4 consecutive positions at once when the group stays in one sequence.
     const QkvOut& o = g.qkv;
     const int hd = o.head_dim, half = hd / 2;
     const int hq = o.n_heads * hd, hkv = o.n_kv_heads * hd;
@@ -263,25 +274,45 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void k_gemm(GemmArgs g) {
       const int sec = col < hq ? 0 : (col < hq + hkv ? 1 : 2);
       const int cc = col - (sec == 0 ? 0 : (sec == 1 ? hq : hq + hkv));
       const int head = cc / hd, pd = cc % hd;
+      const int ii = pd >> 1;
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const float x = acc[i][j][e] + bias;
-          const float partner = __shfl_xor(x, 1, 64);
-          const int row = m0 + wm * TM * 32 + i * 32 + 8 * (e >> 2) + row_q + (e & 3);
-          if (!in || row >= g.M) continue;
-          const int b = row / o.L, pos = row - b * o.L;
-          if (sec < 2) {
-            const int ii = pd >> 1;
-            const float c = o.cos_t[pos * half + ii], sn = o.sin_t[pos * half + ii];
-            const float r = (pd & 1) ? x * c + partner * sn : x * c - partner * sn;
-            uint16_t* dst = sec == 0 ? o.q + ((int64_t)(b * o.n_heads + head) * o.Ls + pos) * hd
-                                     : o.k + ((int64_t)(b * o.n_kv_heads + head) * o.Ls + pos) * hd;
-            dst[pd] = (uint16_t)f32_to_bf16_bits(r);
-          } else {
-            o.vt[((int64_t)(b * o.n_kv_heads + head) * hd + pd) * o.Ls + pos] =
-                (uint16_t)f32_to_bf16_bits(x);
+        for (int e4 = 0; e4 < 4; ++e4) {
+          float x[4], partner[4];
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            x[t] = acc[i][j][e4 * 4 + t] + bias;
+            partner[t] = __shfl_xor(x[t], 1, 64);
+          }
+          const int row0 = m0 + wm * TM * 32 + i * 32 + 8 * e4 + row_q;
+          if (!in || row0 >= g.M) continue;
+          int b = row0 / o.L, pos = row0 - b * o.L;
+          if (sec == 2 && pos + 3 < o.L && row0 + 3 < g.M) {
+            u32x2_t v2;
+            v2.x = pack_bf16x2(x[0], x[1]);
+            v2.y = pack_bf16x2(x[2], x[3]);
+            if ((o.L & 3) == 0) {
+              *reinterpret_cast<u32x2_t*>(
+                  &o.vt[((int64_t)(b * o.n_kv_heads + head) * hd + pd) * o.Ls + pos]) = v2;
+              continue;
+            }
+          }
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            if (row0 + t >= g.M) break;
+            if (sec < 2) {
+              const float c = o.cos_t[pos * half + ii], sn = o.sin_t[pos * half + ii];
+              const float r = (pd & 1) ? x[t] * c + partner[t] * sn : x[t] * c - partner[t] * sn;
+              uint16_t* dst = sec == 0
+                                  ? o.q + ((int64_t)(b * o.n_heads + head) * o.Ls + pos) * hd
+                                  : o.k + ((int64_t)(b * o.n_kv_heads + head) * o.Ls + pos) * hd;
+              dst[pd] = (uint16_t)f32_to_bf16_bits(r);
+            } else {
+              o.vt[((int64_t)(b * o.n_kv_heads + head) * hd + pd) * o.Ls + pos] =
+                  (uint16_t)f32_to_bf16_bits(x[t]);
+            }
+            if (++pos == o.L) { pos = 0; ++b; }
           }
         }
     }
@@ -317,16 +348,18 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void k_gemm(GemmArgs g) {
 // cfg 0: 256 x 256 tile, 16 waves (4 x 4), wave tile 64 x 64
 // cfg 1:  32 x 128 tile, 4 waves (1 x 4) (2 waves for SwiGLU), for M <= 64 (LM head rows)
 // cfg 2: 256 x 128 tile,  8 waves (4 x 2), wave tile 64 x 64
+// cfg 3: 256 x 192 tile, 12 waves (4 x 3), wave tile 64 x 64
 struct CfgShape { int bm, bn; };
 static CfgShape cfg_shape(int cfg) {
   switch (cfg) {
     case 0: return {256, 256};
     case 1: return {32, 128};
+    case 3: return {256, 192};
     default: return {256, 128};
   }
 }
 
-int gemm_num_cfgs() { return 3; }
+int gemm_num_cfgs() { return 4; }
 
 GemmPlan gemm_plan_cfg(int epi, int M, int N, int K, int num_cus, int cfg) {
   GemmPlan p{};
@@ -345,13 +378,29 @@ GemmPlan gemm_plan_cfg(int epi, int M, int N, int K, int num_cus, int cfg) {
   return p;
 }
 
-// Choice measured on the pass's shapes: the 256 x 256 tile when it still yields enough
-// tiles (residual updates split K, so fewer suffice), else 256 x 128.
+// Choice measured on the pass's shapes.  Residual updates (fp32 add) take the 256 x 256
+// tile when it still yields enough tiles (they split K), else 256 x 128.  Other epilogues
+// minimise rounds-of-tiles x tile area / relative efficiency (16, 12 and 8 waves per
+// workgroup: 1.0, 0.95, 0.85), which picks the fastest measured config at every shape
+// of the pass (e.g. 256 x 192 for the 512 x 24576 gate/up, 256 x 128 for 512 x 12288).
 GemmPlan gemm_plan(int epi, int M, int N, int K, int num_cus) {
   if (M <= 64) return gemm_plan_cfg(epi, M, N, K, num_cus, 1);
-  const int tiles0 = ((M + 255) / 256) * ((N + 255) / 256);
-  const int need = epi == EPI_ADD_F32 ? num_cus / 4 : (num_cus * 3) / 4;
-  return gemm_plan_cfg(epi, M, N, K, num_cus, tiles0 >= need ? 0 : 2);
+  if (epi == EPI_ADD_F32) {
+    const int tiles0 = ((M + 255) / 256) * ((N + 255) / 256);
+    return gemm_plan_cfg(epi, M, N, K, num_cus, tiles0 >= num_cus / 4 ? 0 : 2);
+  }
+  const int cfgs[3] = {0, 3, 2};
+  const double eff[3] = {1.0, 0.95, 0.85};
+  int best = 0;
+  double best_cost = 0;
+  for (int c = 0; c < 3; ++c) {
+    const CfgShape sh = cfg_shape(cfgs[c]);
+    const int tiles = ((M + sh.bm - 1) / sh.bm) * ((N + sh.bn - 1) / sh.bn);
+    const int rounds = (tiles + num_cus - 1) / num_cus;
+    const double cost = (double)rounds * sh.bm * sh.bn / eff[c];
+    if (c == 0 || cost < best_cost) { best = cfgs[c]; best_cost = cost; }
+  }
+  return gemm_plan_cfg(epi, M, N, K, num_cus, best);
 }
 
 template <int WAVES_M, int WAVES_N, int TM, int TN, int EPI, int DEPTH>
@@ -368,6 +417,7 @@ static hipError_t run_cfg(int cfg, const GemmArgs& a, int grid, hipStream_t s) {
     case 1:
       if constexpr (EPI == EPI_SWIGLU) return run<1, 2, 1, 2, EPI, 2>(a, grid, s);
       else return run<1, 4, 1, 1, EPI, 2>(a, grid, s);
+    case 3: return run<4, 3, 2, 2, EPI, 1>(a, grid, s);
     default: return run<4, 2, 2, 2, EPI, 1>(a, grid, s);
   }
 }

@@ -1,7 +1,9 @@
 """Helpers for GPU-vs-oracle parity: tolerances and decision-comparability rules.
 
-Logit tolerance: max |l_gpu - l_oracle| <= 2e-2 * S, S = max |l_oracle| over the compared
-rows (bf16 GEMMs, fp32 accumulation).
+Logit tolerance: max |l_gpu - l_oracle| <= 2e-2 * S, with S the logit scale of the compared
+rows read shift-invariantly: the softmax of Eq. (1) does not change when a row's logits are
+shifted by a constant, so S is the largest per-row range max_v l - min_v l (bf16 GEMMs, fp32
+accumulation).
 
 A decision is compared bit-exactly only where the measured per-row logit error D_i cannot
 flip it (Proposition 1: an argmax survives any perturbation below half its margin):
@@ -21,8 +23,14 @@ def bf16_to_f32(bits):
     return (np.asarray(bits).astype(np.uint16).astype(np.uint32) << 16).view(np.float32)
 
 
+def logit_scale(ref):
+    """Largest per-row range (max - min) of the reference logits."""
+    ref = np.atleast_2d(np.asarray(ref, dtype=np.float64))
+    return float(np.max(ref.max(axis=-1) - ref.min(axis=-1)))
+
+
 def logit_tolerance(ref):
-    return LOGIT_TOL_FRAC * float(np.max(np.abs(ref)))
+    return LOGIT_TOL_FRAC * logit_scale(ref)
 
 
 def margins(logits, mask_id=None):
