@@ -52,7 +52,8 @@ typedef enum {
  * softmax attention (grouped kv heads allowed), output projection, RMSNorm,
  * SwiGLU MLP, final RMSNorm and an untied LM head scaled by logit_scale.
  * Limits: head_dim in {64, 128}; n_heads % n_kv_heads == 0; d_model and
- * n_heads*head_dim multiples of 64; vocab >= 2; 0 <= mask_id < vocab. */
+ * n_heads*head_dim multiples of 64; d_model <= 8192; vocab >= 2;
+ * 0 <= mask_id < vocab. */
 typedef struct {
   int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, ffn_dim, vocab, mask_id;
   int32_t qkv_bias; /* 0/1: bias on the q, k and v projections */

@@ -11,13 +11,14 @@
 // column hit distinct banks.
 //
 // Split-K (for outputs with too few tiles to fill the chip): split s of a tile
-// accumulates K-slices [s*nk, (s+1)*nk), stores its fp32 partial tile to a workspace,
-// and takes a ticket on the tile; the last split to arrive adds the partials in split
-// order (0, 1, ..., S-1), so the result does not depend on arrival order, runs the
-// epilogue and resets the ticket.
+// accumulates K-slices [s*nk, (s+1)*nk) and stores its fp32 partial tile (EPI_PART_F32);
+// a row-wise kernel downstream adds the partials in split order, so results do not depend
+// on scheduling, and applies what the output needs next (residual add + RMSNorm, or bias +
+// RoPE + head layout for q/k/v).
 //
 // Epilogues:  EPI_BF16    C = bf16((acc + bias[n]) * scale)
 //             EPI_ADD_F32 C(fp32) += acc            (residual stream update)
+//             EPI_PART_F32  split s stores acc to its own fp32 slab of C
 //             EPI_SWIGLU  weights interleave gate/up rows in groups of 32, so a
 //                         wavefront's two 32-column blocks hold gate and up of the
 //                         same outputs: C = bf16(silu(g) * u), ldc over ffn columns.
@@ -59,7 +60,6 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void k_gemm(GemmArgs g) {
 
   __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * LDK];
   __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BN * LDK];
-  __shared__ int s_last;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WAVES_N, wn = wave % WAVES_N;
@@ -183,59 +183,6 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void k_gemm(GemmArgs g) {
     }
   }
 #undef GEMM_FETCH
-  if (g.splits > 1) {
-    // Deterministic split-K.  Partials of a tile are laid out [split][NACC/4][thread] as
-    // 16-byte vectors, so each store instruction covers 1 KiB contiguously.  They are
-    // written and read with agent-scope coherence (sc1) instead of a release fence, which
-    // would write back the whole L2: completed sc1 stores (vmcnt 0) are visible to any
-    // XCD, then the ticket is taken.
-    const int64_t part_floats = (int64_t)g.splits * NT * NACC;
-    const __amdgpu_buffer_rsrc_t ws_rs = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(g.ws + (int64_t)tile * part_floats), (short)0, (int)(part_floats * 4), 0x00020000);
-    constexpr int SC1 = 16;
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-#pragma unroll
-        for (int e = 0; e < 16; e += 4) {
-          const int q = (i * TN + j) * 4 + e / 4;
-          const f32x4_t v{acc[i][j][e], acc[i][j][e + 1], acc[i][j][e + 2], acc[i][j][e + 3]};
-          __builtin_amdgcn_raw_buffer_store_b128(v, ws_rs, ((split * (NACC / 4) + q) * NT + tid) * 16,
-                                                 0, SC1);
-        }
-    __builtin_amdgcn_s_waitcnt(0);  // every counter drained: the partial stores completed
-    __syncthreads();
-    if (tid == 0)
-      s_last = __hip_atomic_fetch_add(&g.counters[tile], 1, __ATOMIC_RELAXED,
-                                      __HIP_MEMORY_SCOPE_AGENT) == g.splits - 1;
-    __syncthreads();
-    if (!s_last) return;
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
-    for (int sp = 0; sp < g.splits; ++sp) {
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-#pragma unroll
-          for (int e = 0; e < 16; e += 4) {
-            const int q = (i * TN + j) * 4 + e / 4;
-            const f32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(
-                ws_rs, ((sp * (NACC / 4) + q) * NT + tid) * 16, 0, SC1);
-            acc[i][j][e] += v[0];
-            acc[i][j][e + 1] += v[1];
-            acc[i][j][e + 2] += v[2];
-            acc[i][j][e + 3] += v[3];
-          }
-    }
-    if (tid == 0) __hip_atomic_store(&g.counters[tile], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
-
   // epilogue: acc[i][j][e] is C[row, col] with
   //   row = m0 + wm*TM*32 + i*32 + 8*(e/4) + 4*(lane/32) + e%4,  col = n0 + wn*TN*32 + j*32 + lane%32
   const int col_l = lane & 31, row_q = (lane >> 5) * 4;
@@ -331,6 +278,9 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void k_gemm(GemmArgs g) {
           if constexpr (EPI == EPI_ADD_F32) {
             float* C = reinterpret_cast<float*>(g.C);
             C[(int64_t)row * g.ldc + col] += acc[i][j][e];
+          } else if constexpr (EPI == EPI_PART_F32) {
+            float* C = reinterpret_cast<float*>(g.C) + (int64_t)split * g.M * g.ldc;
+            C[(int64_t)row * g.ldc + col] = acc[i][j][e];
           } else {
             uint16_t* C = reinterpret_cast<uint16_t*>(g.C);
             C[(int64_t)row * g.ldc + col] =
@@ -361,46 +311,63 @@ static CfgShape cfg_shape(int cfg) {
 
 int gemm_num_cfgs() { return 4; }
 
-GemmPlan gemm_plan_cfg(int epi, int M, int N, int K, int num_cus, int cfg) {
+// Relative main-loop efficiency of the large-tile configs (16, 12 and 8 waves per workgroup),
+// measured on the pass's shapes.
+static double cfg_eff(int cfg) { return cfg == 0 ? 1.0 : (cfg == 3 ? 0.95 : 0.85); }
+
+GemmPlan gemm_plan_cfg(int M, int N, int K, int cfg, int splits) {
   GemmPlan p{};
   p.cfg = cfg;
   const CfgShape sh = cfg_shape(cfg);
   p.tiles = ((M + sh.bm - 1) / sh.bm) * ((N + sh.bn - 1) / sh.bn);
-  p.splits = 1;
-  if (cfg != 1 && epi == EPI_ADD_F32) {
-    // split the K loop until the grid covers the chip, keeping >= 8 slices per split
-    const int nk = K / BK;
-    while (p.tiles * p.splits < num_cus && p.splits < 8 && nk % (p.splits * 2) == 0 &&
-           nk / (p.splits * 2) >= 8)
-      p.splits *= 2;
-  }
-  p.ws_floats = p.splits > 1 ? (size_t)p.tiles * p.splits * sh.bm * sh.bn : 0;
+  p.splits = splits;
+  p.ws_floats = splits > 1 ? (size_t)splits * M * N : 0;
   return p;
 }
 
-// Choice measured on the pass's shapes.  Residual updates (fp32 add) take the 256 x 256
-// tile when it still yields enough tiles (they split K), else 256 x 128.  Other epilogues
-// minimise rounds-of-tiles x tile area / relative efficiency (16, 12 and 8 waves per
-// workgroup: 1.0, 0.95, 0.85), which picks the fastest measured config at every shape
-// of the pass (e.g. 256 x 192 for the 512 x 24576 gate/up, 256 x 128 for 512 x 12288).
-GemmPlan gemm_plan(int epi, int M, int N, int K, int num_cus) {
-  if (M <= 64) return gemm_plan_cfg(epi, M, N, K, num_cus, 1);
-  if (epi == EPI_ADD_F32) {
-    const int tiles0 = ((M + 255) / 256) * ((N + 255) / 256);
-    return gemm_plan_cfg(epi, M, N, K, num_cus, tiles0 >= num_cus / 4 ? 0 : 2);
-  }
+// Whole-K tiles: minimise rounds-of-tiles x tile area / efficiency, which picks the fastest
+// measured config at every shape of the pass (e.g. 256 x 192 for the 512 x 24576 gate/up,
+// 256 x 128 for 512 x 12288).
+GemmPlan gemm_plan(int M, int N, int K, int num_cus) {
+  if (M <= 64) return gemm_plan_cfg(M, N, K, 1, 1);
   const int cfgs[3] = {0, 3, 2};
-  const double eff[3] = {1.0, 0.95, 0.85};
   int best = 0;
   double best_cost = 0;
   for (int c = 0; c < 3; ++c) {
     const CfgShape sh = cfg_shape(cfgs[c]);
     const int tiles = ((M + sh.bm - 1) / sh.bm) * ((N + sh.bn - 1) / sh.bn);
     const int rounds = (tiles + num_cus - 1) / num_cus;
-    const double cost = (double)rounds * sh.bm * sh.bn / eff[c];
+    const double cost = (double)rounds * sh.bm * sh.bn / cfg_eff(cfgs[c]);
     if (c == 0 || cost < best_cost) { best = cfgs[c]; best_cost = cost; }
   }
-  return gemm_plan_cfg(epi, M, N, K, num_cus, best);
+  return gemm_plan_cfg(M, N, K, best, 1);
+}
+
+// Tiles that may split K (outputs whose consumer folds partials in): estimated time =
+// rounds x per-tile main loop (1.9 MMAC per microsecond per CU at efficiency 1) + partial
+// traffic (written here, read back downstream: ~0.4 us per MiB), over configs {0, 2, 3} and
+// 1, 2, 4 or 8 splits with >= 8 K-slices each.  Splits never exceed the workspace bound.
+GemmPlan gemm_plan_split(int M, int N, int K, int num_cus) {
+  if (M <= 64) return gemm_plan_cfg(M, N, K, 1, 1);
+  const int nk = K / BK;
+  const int cfgs[3] = {0, 3, 2};
+  GemmPlan best{};
+  double best_us = 0;
+  bool have = false;
+  for (int c = 0; c < 3; ++c) {
+    const CfgShape sh = cfg_shape(cfgs[c]);
+    const int tiles = ((M + sh.bm - 1) / sh.bm) * ((N + sh.bn - 1) / sh.bn);
+    for (int sp = 1; sp <= 8; sp *= 2) {
+      if (sp > 1 && (nk % sp != 0 || nk / sp < 8 ||
+                     (size_t)sp * M * N > gemm_ws_floats_bound(num_cus)))
+        continue;
+      const int rounds = (tiles * sp + num_cus - 1) / num_cus;
+      double us = (double)rounds * sh.bm * sh.bn * ((double)K / sp) / cfg_eff(cfgs[c]) / 1.9e6;
+      if (sp > 1) us += 0.4 * (double)sp * M * N * 4.0 / (1 << 20);
+      if (!have || us < best_us) { best = gemm_plan_cfg(M, N, K, cfgs[c], sp); best_us = us; have = true; }
+    }
+  }
+  return best;
 }
 
 template <int WAVES_M, int WAVES_N, int TM, int TN, int EPI, int DEPTH>
@@ -424,8 +391,8 @@ static hipError_t run_cfg(int cfg, const GemmArgs& a, int grid, hipStream_t s) {
 
 hipError_t launch_gemm(int epi, const GemmArgs& in, const GemmPlan& p, hipStream_t s) {
   if (in.M == 0 || in.N == 0) return hipSuccess;
-  if (in.K % (BK * p.splits) != 0) return hipErrorInvalidValue;
-  if (p.splits > 1 && (!in.ws || !in.counters)) return hipErrorInvalidValue;
+  if (p.splits < 1 || in.K % (BK * p.splits) != 0) return hipErrorInvalidValue;
+  if (p.splits > 1 && epi != EPI_PART_F32) return hipErrorInvalidValue;
   GemmArgs a = in;
   a.splits = p.splits;
   const int grid = p.tiles * p.splits;
@@ -434,6 +401,7 @@ hipError_t launch_gemm(int epi, const GemmArgs& in, const GemmPlan& p, hipStream
     case EPI_ADD_F32: return run_cfg<EPI_ADD_F32>(p.cfg, a, grid, s);
     case EPI_SWIGLU: return run_cfg<EPI_SWIGLU>(p.cfg, a, grid, s);
     case EPI_QKV_ROPE: return run_cfg<EPI_QKV_ROPE>(p.cfg, a, grid, s);
+    case EPI_PART_F32: return run_cfg<EPI_PART_F32>(p.cfg, a, grid, s);
   }
   return hipErrorInvalidValue;
 }

@@ -31,13 +31,22 @@ struct RowSel {
 };
 hipError_t launch_rmsnorm(const float* h, const float* w, uint16_t* out, int rows, int d,
                           float eps, RowSel sel, hipStream_t s);
+// h[r, :] += part[0][r, :] + ... + part[splits-1][r, :] (partials [splits][rows][d], summed in
+// split order), then, when out is not null, out[r, :] = bf16(rmsnorm(h[r, :]) * w).
+// d % 4 == 0 and d <= RESIDUAL_NORM_MAX_D.
+constexpr int RESIDUAL_NORM_MAX_D = 8192;
+hipError_t launch_residual_norm(float* h, const float* part, int splits, int rows, int d,
+                                const float* w, uint16_t* out, float eps, hipStream_t s);
 hipError_t launch_state_init(const int32_t* prompt, int B, int P, int G, int mask_id,
                              int32_t* tokens, uint8_t* unresolved, int32_t* prev, int32_t* persist,
                              int32_t* block_idx, int32_t* step_idx, int32_t* passes, int n_blocks,
                              hipStream_t s);
 
 // ---- GEMM: C[M, N] = A[M, K] . W[N, K]^T, bf16 in, fp32 accumulate ---------------------
-enum GemmEpi { EPI_BF16 = 0, EPI_ADD_F32 = 1, EPI_SWIGLU = 2, EPI_QKV_ROPE = 3 };
+enum GemmEpi { EPI_BF16 = 0, EPI_ADD_F32 = 1, EPI_SWIGLU = 2, EPI_QKV_ROPE = 3, EPI_PART_F32 = 4 };
+// EPI_PART_F32: split s of the K loop stores its fp32 partial product to
+// ((float*)C)[s * M * ldc + row * ldc + col]; the partials are folded in by a later kernel
+// (launch_residual_norm), so the GEMM itself takes no tickets.
 // EPI_QKV_ROPE: columns [0, H*hd) are q heads, then Hkv*hd k heads, then Hkv*hd v heads;
 // q and k weight rows are pair-interleaved per head (ROW_ROPE_PAIR).  Adds the bias,
 // rotates q and k (rotate-half RoPE at position row % L), and writes q [B, H, Ls, hd],
@@ -55,21 +64,23 @@ struct GemmArgs {
   const float* bias;   // EPI_BF16: per-column bias (or null)
   float scale;         // EPI_BF16: multiplier after the bias
   int splits;          // set by launch_gemm from the plan
-  float* ws;           // split-K partials (GemmPlan::ws_floats floats)
-  int32_t* counters;   // split-K tickets, one per tile, zero on entry and exit
   QkvOut qkv;          // EPI_QKV_ROPE destinations
 };
 struct GemmPlan {
   int cfg, tiles, splits;
-  size_t ws_floats;
+  size_t ws_floats;    // EPI_PART_F32 partial floats (splits * M * N) when splits > 1
 };
-// Tile configuration and K split for one GEMM shape.  Split-K workspace never exceeds
-// gemm_ws_floats_bound(num_cus) floats and num_cus tickets.
-GemmPlan gemm_plan(int epi, int M, int N, int K, int num_cus);
-GemmPlan gemm_plan_cfg(int epi, int M, int N, int K, int num_cus, int cfg);
+// Whole-K plan for any epilogue; split plan (EPI_PART_F32 when splits > 1, else any
+// epilogue) never needs more than gemm_ws_floats_bound(num_cus) partial floats.
+GemmPlan gemm_plan(int M, int N, int K, int num_cus);
+GemmPlan gemm_plan_split(int M, int N, int K, int num_cus);
+GemmPlan gemm_plan_cfg(int M, int N, int K, int cfg, int splits);
 int gemm_num_cfgs();
 inline size_t gemm_ws_floats_bound(int num_cus) { return (size_t)2 * num_cus * 256 * 256; }
 hipError_t launch_gemm(int epi, const GemmArgs& a, const GemmPlan& p, hipStream_t s);
+// EPI_PART_F32 partials [splits][M][N] of the QKV projection -> the EPI_QKV_ROPE outputs.
+hipError_t launch_qkv_finish(const float* part, int splits, int M, int N, const float* bias,
+                             const QkvOut& o, hipStream_t s);
 
 // ---- attention ---------------------------------------------------------------------------
 hipError_t launch_attention(const uint16_t* q, const uint16_t* k, const uint16_t* vt,

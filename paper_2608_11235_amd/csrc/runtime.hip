@@ -69,7 +69,7 @@ struct cora_model {
   int32_t* tickets = nullptr;
   int num_cus = 256;
   float* splitk_ws = nullptr;
-  int32_t* splitk_cnt = nullptr;
+  size_t splitk_ws_floats = 0;
   // decode state owned for cora_block_decode
   int32_t *s_tokens = nullptr, *s_prev = nullptr, *s_persist = nullptr, *s_block = nullptr;
   int32_t *s_step = nullptr, *s_top1 = nullptr, *s_done = nullptr, *s_passes = nullptr;
@@ -97,6 +97,8 @@ static cora_status validate_cfg(const cora_model_cfg& c) {
     return fail(CORA_ERR_UNSUPPORTED, "n_heads must be a multiple of n_kv_heads");
   if (c.d_model % 64 != 0 || (c.n_heads * c.head_dim) % 64 != 0)
     return fail(CORA_ERR_UNSUPPORTED, "d_model and n_heads*head_dim must be multiples of 64");
+  if (c.d_model > RESIDUAL_NORM_MAX_D)
+    return fail(CORA_ERR_UNSUPPORTED, "d_model must not exceed 8192");
   if (!(c.rms_eps > 0.f) || !(c.rope_theta > 0.f) || !isfinite(c.logit_scale) ||
       !(c.init_std >= 0.0))
     return fail(CORA_ERR_INVALID_ARG, "rms_eps, rope_theta must be > 0; logit_scale finite");
@@ -158,7 +160,7 @@ extern "C" cora_status cora_model_create(const cora_model_cfg* cfg, uint64_t see
       m->num_cus = cus;
   }
   const size_t skw = gemm_ws_floats_bound(m->num_cus);
-  size_t wsb = align_up(skw * 4) + align_up((size_t)m->num_cus * 4) + align_up(M * d * 4) + align_up(M * (size_t)(d > m->hq ? d : m->hq) * 2) +
+  size_t wsb = align_up(skw * 4) + align_up(M * d * 4) + align_up(M * (size_t)(d > m->hq ? d : m->hq) * 2) +
                align_up(Ms * m->hq * 2) + 2 * align_up(Ms * m->hkv * 2) +
                align_up(M * m->hq * 2) + align_up(M * m->f_pad * 2) + align_up(rows * V * 2) +
                2 * align_up((size_t)m->max_seq_pad * (hd / 2) * 4) + align_up(max_batch * 4) +
@@ -194,7 +196,7 @@ extern "C" cora_status cora_model_create(const cora_model_cfg* cfg, uint64_t see
   }
   Arena a{(char*)m->ws_mem, 0, wsb};
   m->splitk_ws = a.take<float>(skw);
-  m->splitk_cnt = a.take<int32_t>(m->num_cus);
+  m->splitk_ws_floats = skw;
   m->h = a.take<float>(M * d);
   m->a = a.take<uint16_t>(M * (d > m->hq ? d : m->hq));
   m->q = a.take<uint16_t>(Ms * m->hq);
@@ -227,7 +229,6 @@ extern "C" cora_status cora_model_create(const cora_model_cfg* cfg, uint64_t see
   auto st = [&]() -> cora_status {
     HIP_TRY(hipMemsetAsync(m->weight_mem, 0, wb, s));
     HIP_TRY(hipMemsetAsync(m->tickets, 0, max_batch * sizeof(int32_t), s));
-    HIP_TRY(hipMemsetAsync(m->splitk_cnt, 0, m->num_cus * sizeof(int32_t), s));
     const double sd = cfg->init_std;
     HIP_TRY(hipMemsetAsync(m->ws_mem, 0, wsb, s));  // finite zeros in every padding region
     HIP_TRY(launch_init_bf16(m->embed, seed, 1, V, d, d, ROW_IDENTITY, 0, sd, hd, s));
@@ -329,11 +330,48 @@ static cora_status timed_event(cora_model* m, hipStream_t s) {
 
 // ---- one dense pass ----------------------------------------------------------------------
 static cora_status gemm(cora_model* m, int epi, const GemmArgs& g, hipStream_t s) {
-  const GemmPlan p = gemm_plan(epi, g.M, g.N, g.K, m->num_cus);
-  GemmArgs a = g;
-  a.ws = m->splitk_ws;
-  a.counters = m->splitk_cnt;
-  HIP_TRY(launch_gemm(epi, a, p, s));
+  HIP_TRY(launch_gemm(epi, g, gemm_plan(g.M, g.N, g.K, m->num_cus), s));
+  return CORA_OK;
+}
+
+// Split-K GEMM into the partial workspace (plan p with p.splits > 1).
+static cora_status gemm_partials(cora_model* m, GemmArgs g, const GemmPlan& p, hipStream_t s) {
+  if (p.ws_floats > m->splitk_ws_floats)
+    return fail(CORA_ERR_UNSUPPORTED, "shape exceeds the split-K workspace");
+  g.C = m->splitk_ws;
+  g.ldc = g.N;
+  HIP_TRY(launch_gemm(EPI_PART_F32, g, p, s));
+  return CORA_OK;
+}
+
+// QKV projection with bias, RoPE and head layout, whole-K or split-K.
+static cora_status qkv_gemm(cora_model* m, const GemmArgs& g, hipStream_t s) {
+  const GemmPlan p = gemm_plan_split(g.M, g.N, g.K, m->num_cus);
+  if (p.splits == 1) {
+    HIP_TRY(launch_gemm(EPI_QKV_ROPE, g, p, s));
+    return CORA_OK;
+  }
+  if (cora_status st = gemm_partials(m, g, p, s)) return st;
+  HIP_TRY(launch_qkv_finish(m->splitk_ws, p.splits, g.M, g.N, g.bias, g.qkv, s));
+  return CORA_OK;
+}
+
+// Residual update h += A . W^T; when norm_out is given it then receives rmsnorm(h) for the
+// next GEMM.  Split-K plans store per-split partials and fold them into h, together with the
+// norm, in one row-wise kernel.
+static cora_status residual_gemm(cora_model* m, GemmArgs g, uint16_t* norm_out, hipStream_t s) {
+  const auto& c = m->cfg;
+  const GemmPlan p = gemm_plan_split(g.M, g.N, g.K, m->num_cus);
+  float* h = reinterpret_cast<float*>(g.C);
+  if (p.splits == 1) {
+    HIP_TRY(launch_gemm(EPI_ADD_F32, g, p, s));
+    const RowSel all{0, 0, 0, 0, 0, 0, 0, nullptr};
+    if (norm_out) HIP_TRY(launch_rmsnorm(h, m->ones, norm_out, g.M, g.N, c.rms_eps, all, s));
+    return CORA_OK;
+  }
+  if (cora_status st = gemm_partials(m, g, p, s)) return st;
+  HIP_TRY(launch_residual_norm(h, m->splitk_ws, p.splits, g.M, g.N, m->ones, norm_out,
+                               c.rms_eps, s));
   return CORA_OK;
 }
 
@@ -342,17 +380,19 @@ static cora_status run_layers(cora_model* m, const int32_t* tokens, int B, int L
   const int d = c.d_model, M = B * L, Ls = round_up(L, 64);
   HIP_TRY(launch_embed(tokens, m->embed, m->h, M, d, c.vocab, s));
   const RowSel all{0, L, 0, 0, 0, 0, 0, nullptr};
-  for (const auto& ly : m->layers) {
-    HIP_TRY(launch_rmsnorm(m->h, m->ones, m->a, M, d, c.rms_eps, all, s));
+  HIP_TRY(launch_rmsnorm(m->h, m->ones, m->a, M, d, c.rms_eps, all, s));
+  const size_t n_layers = m->layers.size();
+  for (size_t l = 0; l < n_layers; ++l) {
+    const auto& ly = m->layers[l];
+    // m->a holds rmsnorm(h) of this layer's input
     GemmArgs g{m->a, d, ly.wqkv, d, M, m->qkv_n, d, nullptr, 0, ly.bqkv, 1.0f};
     g.qkv = QkvOut{m->q, m->k, m->vt, m->rope_cos, m->rope_sin, L, Ls, c.n_heads, c.n_kv_heads,
                    c.head_dim};
-    if (cora_status st = gemm(m, EPI_QKV_ROPE, g, s)) return st;
+    if (cora_status st = qkv_gemm(m, g, s)) return st;
     HIP_TRY(launch_attention(m->q, m->k, m->vt, m->attn, B, L, Ls, c.n_heads, c.n_kv_heads,
                              c.head_dim, s));
     g = GemmArgs{m->attn, m->hq, ly.wo, m->hq, M, d, m->hq, m->h, d, nullptr, 1.0f};
-    if (cora_status st = gemm(m, EPI_ADD_F32, g, s)) return st;
-    HIP_TRY(launch_rmsnorm(m->h, m->ones, m->a, M, d, c.rms_eps, all, s));
+    if (cora_status st = residual_gemm(m, g, m->a, s)) return st;
     g = GemmArgs{m->a, d, ly.wgu, d, M, 2 * m->f_pad, d, m->u, m->f_pad, nullptr, 1.0f};
     if (m->timing)
       if (cora_status st = timed_event(m, s)) return st;
@@ -360,7 +400,8 @@ static cora_status run_layers(cora_model* m, const int32_t* tokens, int B, int L
     if (m->timing)
       if (cora_status st = timed_event(m, s)) return st;
     g = GemmArgs{m->u, m->f_pad, ly.wd, m->f_pad, M, d, m->f_pad, m->h, d, nullptr, 1.0f};
-    if (cora_status st = gemm(m, EPI_ADD_F32, g, s)) return st;
+    // the last layer's output is normalised only on the rows the LM head reads
+    if (cora_status st = residual_gemm(m, g, l + 1 < n_layers ? m->a : nullptr, s)) return st;
   }
   return CORA_OK;
 }

@@ -17,6 +17,9 @@ pytestmark = pytest.mark.gpu
 
 MINI_GQA = si.ModelSpec("mini-gqa", 2, 256, 4, 2, 64, 300, 1000, 999, True, 1e-6, 1e6, 6.0)
 MINI_HD128 = si.ModelSpec("mini-hd128", 1, 256, 2, 1, 128, 512, 777, 5, True, 1e-6, 1e6, 6.0)
+# wide enough (K >= 1024) that the QKV, output and down projections split K: partial
+# workspace + the QKV finish and residual/norm kernels instead of whole-K epilogues
+MID_SPLIT = si.ModelSpec("mid-split", 2, 1024, 8, 2, 128, 2816, 1000, 999, True, 1e-6, 1e6, 6.0)
 
 
 def _tensors(spec):
@@ -79,6 +82,13 @@ def test_tiny_forward(B, L, row_begin, n_rows):
 def test_gqa_bias_forward(spec):
     require_gpu()
     _check_logits(spec, 2, 100, 10, 40)
+
+
+@pytest.mark.parametrize("B,L,row_begin,n_rows", [(2, 130, 60, 40), (1, 256, 128, 32)])
+def test_split_k_forward(B, L, row_begin, n_rows):
+    """L = 130: row groups of 4 straddle two sequences (per-row v path); L = 256: vector v."""
+    require_gpu()
+    _check_logits(MID_SPLIT, B, L, row_begin, n_rows)
 
 
 def test_forward_deterministic():
