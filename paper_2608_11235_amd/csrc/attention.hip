@@ -2,10 +2,15 @@
 //
 // Inputs: q [B, H, Ls, hd], k [B, Hkv, Ls, hd] (RoPE applied), vt [B, Hkv, hd, Ls]
 // (v transposed), rows >= L zero.  Output: o [B * L, H * hd] bf16.
-// One workgroup = 64 queries of one head (4 wavefronts x 16 queries); key tiles of 64
-// are staged in LDS, double buffered: the next tile's loads are in flight in registers
-// while the current tile is multiplied out of LDS (one barrier per tile).  Everything is computed transposed with
-// v_mfma_f32_16x16x32_bf16 so that a query's softmax statistics never leave its lanes:
+// One workgroup = 64 queries of one head (4 wavefronts x 16 queries) times SPLIT parts of
+// the key range: with SPLIT = 2 a second group of 4 wavefronts runs the same queries over
+// the second half of the key tiles, and the two partial softmax states (max, sum, O) are
+// merged through LDS at the end.  Small grids (B * H * L / 64 below two workgroups per CU)
+// use SPLIT = 2, which doubles the wavefronts per SIMD and halves each one's serial chain.
+// Key tiles of 64 are staged in LDS, double buffered: the next tile's loads are in flight
+// in registers while the current tile is multiplied out of LDS (one barrier per tile).
+// Everything is computed transposed with v_mfma_f32_16x16x32_bf16 so that a query's
+// softmax statistics never leave its lanes:
 //   S^T = K Q^T   (A = K tile from LDS, B = Q^T held in registers)
 //   O^T = V^T P^T (A = V^T tile from LDS, B = P^T straight from the S^T registers)
 // In S^T a lane holds keys 16kb + 4(lane/16) + i of query lane%16; feeding those
@@ -16,8 +21,8 @@
 
 namespace cora {
 
-template <int HD>
-__global__ __launch_bounds__(256) void k_attention(const uint16_t* __restrict__ q,
+template <int HD, int SPLIT>
+__global__ __launch_bounds__(256 * SPLIT) void k_attention(const uint16_t* __restrict__ q,
                                                    const uint16_t* __restrict__ k,
                                                    const uint16_t* __restrict__ vt,
                                                    uint16_t* __restrict__ out, int L, int Ls,
@@ -26,12 +31,14 @@ __global__ __launch_bounds__(256) void k_attention(const uint16_t* __restrict__ 
   constexpr int LDKS = HD + 8;    // padded LDS rows
   constexpr int LDVS = KT + 8;
   constexpr int CK = KT * HD / 8 / 256;  // 16-byte chunks per thread per tile (K and V^T each)
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][KT * LDKS];
-  __shared__ __attribute__((aligned(16))) uint16_t Vs[2][HD * LDVS];
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][SPLIT][KT * LDKS];
+  __shared__ __attribute__((aligned(16))) uint16_t Vs[2][SPLIT][HD * LDVS];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int part = wave >> 2;                // which part of the key range
+  const int tl = tid & 255, tpart = tid >> 8;  // loader thread: its index and part
   const int bh = blockIdx.y, b = bh / H, h = bh % H, kvh = h / (H / Hkv);
-  const int q0 = blockIdx.x * 64 + wave * 16;
+  const int q0 = blockIdx.x * 64 + (wave & 3) * 16;
   const int g = lane >> 4, r16 = lane & 15;
 
   const uint16_t* qh = q + ((int64_t)(b * H + h) * Ls) * HD;
@@ -48,12 +55,12 @@ __global__ __launch_bounds__(256) void k_attention(const uint16_t* __restrict__ 
   for (int d = 0; d < HD / 16; ++d) o[d] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_part = 0.f;
 
-  // K tile [64 keys][HD] and V^T tile [HD][64 keys]: chunk c of this thread
+  // K tile [64 keys][HD] and V^T tile [HD][64 keys] of part tpart: chunk c of this thread
   u32x4_t rk[CK], rv[CK];
   auto fetch = [&](int key0) {
 #pragma unroll
     for (int i = 0; i < CK; ++i) {
-      const int c = tid + i * 256;
+      const int c = tl + i * 256;
       const int kr = c / (HD / 8), kc = (c % (HD / 8)) * 8;
       rk[i] = *reinterpret_cast<const u32x4_t*>(kh + (int64_t)(key0 + kr) * HD + kc);
       const int vr = c / (KT / 8), vc = (c % (KT / 8)) * 8;
@@ -63,78 +70,112 @@ __global__ __launch_bounds__(256) void k_attention(const uint16_t* __restrict__ 
   auto stash = [&](int buf) {
 #pragma unroll
     for (int i = 0; i < CK; ++i) {
-      const int c = tid + i * 256;
+      const int c = tl + i * 256;
       const int kr = c / (HD / 8), kc = (c % (HD / 8)) * 8;
-      *reinterpret_cast<u32x4_t*>(&Ks[buf][kr * LDKS + kc]) = rk[i];
+      *reinterpret_cast<u32x4_t*>(&Ks[buf][tpart][kr * LDKS + kc]) = rk[i];
       const int vr = c / (KT / 8), vc = (c % (KT / 8)) * 8;
-      *reinterpret_cast<u32x4_t*>(&Vs[buf][vr * LDVS + vc]) = rv[i];
+      *reinterpret_cast<u32x4_t*>(&Vs[buf][tpart][vr * LDVS + vc]) = rv[i];
     }
   };
 
+  // part p owns key tiles [p * per, min((p + 1) * per, n_tiles)); iteration j works on
+  // tile p * per + j of every part, and parts that ran out skip the work but keep the
+  // barriers
   const int n_tiles = (L + KT - 1) / KT;
-  fetch(0);
+  const int per = (n_tiles + SPLIT - 1) / SPLIT;
+  const bool load0 = tpart * per < n_tiles;
+  if (load0) fetch(tpart * per * KT);
   stash(0);
   __syncthreads();
-  for (int kt = 0; kt < n_tiles; ++kt) {
-    const int buf = kt & 1, key0 = kt * KT;
-    if (kt + 1 < n_tiles) fetch(key0 + KT);  // next tile in flight during this one
-
-    f32x4_t st[4];
+  for (int j = 0; j < per; ++j) {
+    const int buf = j & 1, kt = part * per + j, key0 = kt * KT;
+    const int next = tpart * per + j + 1;  // this thread's next tile to load
+    if (j + 1 < per && next < n_tiles) fetch(next * KT);  // in flight during this tile
+    if (kt < n_tiles) {
+      f32x4_t st[4];
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      st[kb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      for (int kb = 0; kb < 4; ++kb) {
+        st[kb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int kk = 0; kk < HD / 32; ++kk) {
-        const bf16x8_t a = as_bf16x8(
-            *reinterpret_cast<const u32x4_t*>(&Ks[buf][(kb * 16 + r16) * LDKS + kk * 32 + g * 8]));
-        st[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[kk], st[kb], 0, 0, 0);
+        for (int kk = 0; kk < HD / 32; ++kk) {
+          const bf16x8_t a = as_bf16x8(
+              *reinterpret_cast<const u32x4_t*>(&Ks[buf][part][(kb * 16 + r16) * LDKS + kk * 32 + g * 8]));
+          st[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[kk], st[kb], 0, 0, 0);
+        }
+      }
+      float tmax = -INFINITY;
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int key = key0 + kb * 16 + g * 4 + i;
+          const float v = key < L ? st[kb][i] * scale_log2 : -INFINITY;
+          st[kb][i] = v;
+          tmax = fmaxf(tmax, v);
+        }
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+      const float m_new = fmaxf(m_run, tmax);
+      const float alpha = exp2f(m_run - m_new);
+      m_run = m_new;
+      l_part *= alpha;
+#pragma unroll
+      for (int d = 0; d < HD / 16; ++d) o[d] *= alpha;
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float p = exp2f(st[kb][i] - m_new);
+          st[kb][i] = p;
+          l_part += p;
+        }
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        u32x4_t pb;
+        pb.x = pack_bf16x2(st[2 * ks][0], st[2 * ks][1]);
+        pb.y = pack_bf16x2(st[2 * ks][2], st[2 * ks][3]);
+        pb.z = pack_bf16x2(st[2 * ks + 1][0], st[2 * ks + 1][1]);
+        pb.w = pack_bf16x2(st[2 * ks + 1][2], st[2 * ks + 1][3]);
+        const bf16x8_t bfrag = as_bf16x8(pb);
+#pragma unroll
+        for (int d = 0; d < HD / 16; ++d) {
+          const uint16_t* vrow = &Vs[buf][part][(d * 16 + r16) * LDVS + ks * 32 + g * 4];
+          const u32x2_t lo = *reinterpret_cast<const u32x2_t*>(vrow);
+          const u32x2_t hi = *reinterpret_cast<const u32x2_t*>(vrow + 16);
+          const u32x4_t av = u32x4_t{lo.x, lo.y, hi.x, hi.y};
+          o[d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(av), bfrag, o[d], 0, 0, 0);
+        }
       }
     }
-    float tmax = -INFINITY;
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int key = key0 + kb * 16 + g * 4 + i;
-        const float v = key < L ? st[kb][i] * scale_log2 : -INFINITY;
-        st[kb][i] = v;
-        tmax = fmaxf(tmax, v);
-      }
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-    const float m_new = fmaxf(m_run, tmax);
-    const float alpha = exp2f(m_run - m_new);
-    m_run = m_new;
-    l_part *= alpha;
-#pragma unroll
-    for (int d = 0; d < HD / 16; ++d) o[d] *= alpha;
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float p = exp2f(st[kb][i] - m_new);
-        st[kb][i] = p;
-        l_part += p;
-      }
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      u32x4_t pb;
-      pb.x = pack_bf16x2(st[2 * ks][0], st[2 * ks][1]);
-      pb.y = pack_bf16x2(st[2 * ks][2], st[2 * ks][3]);
-      pb.z = pack_bf16x2(st[2 * ks + 1][0], st[2 * ks + 1][1]);
-      pb.w = pack_bf16x2(st[2 * ks + 1][2], st[2 * ks + 1][3]);
-      const bf16x8_t bfrag = as_bf16x8(pb);
-#pragma unroll
-      for (int d = 0; d < HD / 16; ++d) {
-        const uint16_t* vrow = &Vs[buf][(d * 16 + r16) * LDVS + ks * 32 + g * 4];
-        const u32x2_t lo = *reinterpret_cast<const u32x2_t*>(vrow);
-        const u32x2_t hi = *reinterpret_cast<const u32x2_t*>(vrow + 16);
-        const u32x4_t av = u32x4_t{lo.x, lo.y, hi.x, hi.y};
-        o[d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(av), bfrag, o[d], 0, 0, 0);
-      }
-    }
-    if (kt + 1 < n_tiles) stash(buf ^ 1);
+    if (j + 1 < per) stash(buf ^ 1);
     __syncthreads();
+  }
+
+  if constexpr (SPLIT == 2) {
+    // merge the second part's (max, partial sums, O) into the first part's wavefronts;
+    // the K tiles' LDS is free after the loop's last barrier
+    constexpr int NF = 2 + 4 * (HD / 16);
+    float* comb = reinterpret_cast<float*>(&Ks[0][0][0]);
+    static_assert(sizeof(Ks) >= 4 * NF * 64 * sizeof(float), "merge buffer");
+    const int slot = (wave & 3) * NF * 64 + lane;
+    if (part == 1) {
+      comb[slot] = m_run;
+      comb[slot + 64] = l_part;
+#pragma unroll
+      for (int d = 0; d < HD / 16; ++d)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) comb[slot + (2 + 4 * d + i) * 64] = o[d][i];
+    }
+    __syncthreads();
+    if (part == 1) return;
+    const float m1 = comb[slot], l1 = comb[slot + 64];
+    const float m = fmaxf(m_run, m1);
+    const float a0 = exp2f(m_run - m), a1 = exp2f(m1 - m);
+    l_part = l_part * a0 + l1 * a1;
+#pragma unroll
+    for (int d = 0; d < HD / 16; ++d)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) o[d][i] = o[d][i] * a0 + comb[slot + (2 + 4 * d + i) * 64] * a1;
   }
 
   float l = l_part;
@@ -156,17 +197,23 @@ __global__ __launch_bounds__(256) void k_attention(const uint16_t* __restrict__ 
 
 hipError_t launch_attention(const uint16_t* q, const uint16_t* k, const uint16_t* vt,
                             uint16_t* out, int B, int L, int Ls, int H, int Hkv, int hd,
-                            hipStream_t s) {
+                            int num_cus, hipStream_t s) {
   const float scale_log2 = 1.4426950408889634f / sqrtf((float)hd);
   const dim3 grid(Ls / 64, B * H);
-  if (hd == 128)
-    hipLaunchKernelGGL(k_attention<128>, grid, dim3(256), 0, s, q, k, vt, out, L, Ls, H, Hkv,
-                       scale_log2);
-  else if (hd == 64)
-    hipLaunchKernelGGL(k_attention<64>, grid, dim3(256), 0, s, q, k, vt, out, L, Ls, H, Hkv,
-                       scale_log2);
-  else
+  const bool split = (int64_t)grid.x * grid.y < 2 * (int64_t)num_cus;
+#define ATTN(HD_, SP_)                                                                     \
+  hipLaunchKernelGGL((k_attention<HD_, SP_>), grid, dim3(256 * SP_), 0, s, q, k, vt, out, L, \
+                     Ls, H, Hkv, scale_log2)
+  if (hd == 128) {
+    if (split) ATTN(128, 2);
+    else ATTN(128, 1);
+  } else if (hd == 64) {
+    if (split) ATTN(64, 2);
+    else ATTN(64, 1);
+  } else {
     return hipErrorInvalidValue;
+  }
+#undef ATTN
   return hipGetLastError();
 }
 

@@ -85,7 +85,7 @@ hipError_t launch_qkv_finish(const float* part, int splits, int M, int N, const 
 // ---- attention ---------------------------------------------------------------------------
 hipError_t launch_attention(const uint16_t* q, const uint16_t* k, const uint16_t* vt,
                             uint16_t* out, int B, int L, int Ls, int H, int Hkv, int hd,
-                            hipStream_t s);
+                            int num_cus, hipStream_t s);
 
 // ---- vocab / gate (K9) -------------------------------------------------------------------
 struct VocabGateArgs {

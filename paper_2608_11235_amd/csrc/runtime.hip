@@ -390,7 +390,7 @@ static cora_status run_layers(cora_model* m, const int32_t* tokens, int B, int L
                    c.head_dim};
     if (cora_status st = qkv_gemm(m, g, s)) return st;
     HIP_TRY(launch_attention(m->q, m->k, m->vt, m->attn, B, L, Ls, c.n_heads, c.n_kv_heads,
-                             c.head_dim, s));
+                             c.head_dim, m->num_cus, s));
     g = GemmArgs{m->attn, m->hq, ly.wo, m->hq, M, d, m->hq, m->h, d, nullptr, 1.0f};
     if (cora_status st = residual_gemm(m, g, m->a, s)) return st;
     g = GemmArgs{m->a, d, ly.wgu, d, M, 2 * m->f_pad, d, m->u, m->f_pad, nullptr, 1.0f};

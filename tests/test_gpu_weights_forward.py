@@ -72,8 +72,10 @@ def test_lm_head_only(n_rows):
 
 
 @pytest.mark.parametrize("B,L,row_begin,n_rows", [(1, 96, 32, 32), (1, 96, 0, 96), (2, 37, 5, 30),
-                                                  (3, 130, 64, 64)])
+                                                  (3, 130, 64, 64), (16, 512, 250, 40)])
 def test_tiny_forward(B, L, row_begin, n_rows):
+    """Small grids take the key-split attention (two wavefront groups per query tile);
+    B = 16, L = 512 has 512 query-tile workgroups and takes the unsplit one."""
     require_gpu()
     _check_logits(si.TINY, B, L, row_begin, n_rows)
 
