@@ -109,21 +109,20 @@ def vocab_gate_roofline(iters=20):
     import torch
 
     import seeded_inputs as si
-    from paper_2608_11235_amd import DecodeState, Gate, Sched, vocab_gate, vocab_gate_workspace
+    from paper_2608_11235_amd import DecodeState, Gate, Sched, vocab_gate
     w = si.vocab_gate_workload(seed=2)
     Bv, R, V = w.logits_bits.shape
     logits = torch.from_numpy(w.logits_bits.view(np.int16)).cuda()
     L = w.state["tokens"].shape[1]
     st = DecodeState.from_host(w.state, w.prompt_len, L - w.prompt_len, R, w.block_len)
-    ws = vocab_gate_workspace(Bv)
     sc, gt = Sched(w.block_len, w.steps_per_block), Gate(DELTA_P, M_REQ, True)
     for _ in range(3):
-        vocab_gate(logits, R, 0, V, w.mask_id, st, 1, sc, gt, ws)
+        vocab_gate(logits, R, 0, V, w.mask_id, st, 1, sc, gt)
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
     for _ in range(iters):
-        vocab_gate(logits, R, 0, V, w.mask_id, st, 1, sc, gt, ws)
+        vocab_gate(logits, R, 0, V, w.mask_id, st, 1, sc, gt)
     e1.record()
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / iters

@@ -153,15 +153,13 @@ cora_status cora_denoise_step(cora_model *model, cora_state *state, const cora_s
  * k highest-confidence unresolved positions (ties: lower position) fixed
  * (k = k_transfer if >= 0, else the schedule's k_s), the gate on the rest,
  * commit of both sets, and the block/step advance once the block is empty.
- * A fixed row_begin must cover the whole generation region.
- * d_workspace: at least cora_vocab_gate_workspace_bytes(B) bytes of device
- * memory, zero before the first call; every call leaves it zero again.
- * Calls sharing one workspace must not overlap.  Asynchronous. */
-size_t cora_vocab_gate_workspace_bytes(int32_t B);
+ * A fixed row_begin must cover the whole generation region.  Two kernel
+ * launches on hip_stream (row reduction, then the decision rules); calls on one
+ * state must not overlap.  Asynchronous. */
 cora_status cora_vocab_gate(const uint16_t *d_logits, int32_t n_rows, int32_t row_begin,
                             int32_t V, int32_t mask_id, cora_state *state, int32_t k_transfer,
                             const cora_sched_cfg *sched, const cora_gate_cfg *gate,
-                            void *d_workspace, size_t workspace_bytes, void *hip_stream);
+                            void *hip_stream);
 
 /* Gated block decode of B prompts (d_prompt int32 [B, prompt_len], device):
  * the canvas starts as prompt + gen_len masks, rows decode independently and

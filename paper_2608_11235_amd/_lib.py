@@ -46,10 +46,8 @@ EXPORTS = {
     "cora_forward_logits": (c_i32, [c_vp, c_vp, c_i32, c_i32, c_i32, c_i32, c_vp, c_vp]),
     "cora_denoise_step": (c_i32, [c_vp, ctypes.POINTER(State), ctypes.POINTER(SchedCfg),
                                   ctypes.POINTER(GateCfg), c_vp]),
-    "cora_vocab_gate_workspace_bytes": (c_sz, [c_i32]),
     "cora_vocab_gate": (c_i32, [c_vp, c_i32, c_i32, c_i32, c_i32, ctypes.POINTER(State), c_i32,
-                                ctypes.POINTER(SchedCfg), ctypes.POINTER(GateCfg), c_vp, c_sz,
-                                c_vp]),
+                                ctypes.POINTER(SchedCfg), ctypes.POINTER(GateCfg), c_vp]),
     "cora_block_decode": (c_i32, [c_vp, c_vp, c_i32, c_i32, c_i32, ctypes.POINTER(SchedCfg),
                                   ctypes.POINTER(GateCfg), c_vp, c_vp, c_vp, c_vp]),
     "cora_model_copy_tensor": (c_i32, [c_vp, c_i32, c_vp, c_sz]),

@@ -181,16 +181,10 @@ class Model:
         return w.value, ws.value
 
 
-def vocab_gate_workspace(B, device="cuda"):
-    n = _lib.load().cora_vocab_gate_workspace_bytes(B)
-    return torch.zeros(max(n, 4) // 4, dtype=torch.int32, device=device)
-
-
 def vocab_gate(logits, n_rows, row_begin, V, mask_id, state: DecodeState, k_transfer,
-               sched: Sched, gate: Gate, workspace, stream=None):
+               sched: Sched, gate: Gate, stream=None):
     st, sc, gt = state.c(), sched.c(), gate.c()
     check(_lib.load().cora_vocab_gate(ptr(logits), n_rows, row_begin, V, mask_id,
                                        ctypes.byref(st), k_transfer, ctypes.byref(sc),
-                                       ctypes.byref(gt), ptr(workspace),
-                                       workspace.numel() * workspace.element_size(),
-                                       stream_handle(stream)), "cora_vocab_gate")
+                                       ctypes.byref(gt), stream_handle(stream)),
+          "cora_vocab_gate")

@@ -96,7 +96,6 @@ struct VocabGateArgs {
   int B, L, prompt_len, block_len, steps_per_block, n_blocks;
   int k_transfer;  // >= 0 fixed k, < 0: schedule
   float delta_p; int m_req; int gate_enabled;
-  int32_t* tickets;  // [B], zero on entry and exit
 };
 hipError_t launch_vocab_gate(const VocabGateArgs& a, hipStream_t s);
 

@@ -66,7 +66,6 @@ struct cora_model {
   uint16_t *a = nullptr, *q = nullptr, *k = nullptr, *vt = nullptr;
   uint16_t *attn = nullptr, *u = nullptr, *logits = nullptr;
   float *rope_cos = nullptr, *rope_sin = nullptr;
-  int32_t* tickets = nullptr;
   int num_cus = 256;
   float* splitk_ws = nullptr;
   size_t splitk_ws_floats = 0;
@@ -163,7 +162,7 @@ extern "C" cora_status cora_model_create(const cora_model_cfg* cfg, uint64_t see
   size_t wsb = align_up(skw * 4) + align_up(M * d * 4) + align_up(M * (size_t)(d > m->hq ? d : m->hq) * 2) +
                align_up(Ms * m->hq * 2) + 2 * align_up(Ms * m->hkv * 2) +
                align_up(M * m->hq * 2) + align_up(M * m->f_pad * 2) + align_up(rows * V * 2) +
-               2 * align_up((size_t)m->max_seq_pad * (hd / 2) * 4) + align_up(max_batch * 4) +
+               2 * align_up((size_t)m->max_seq_pad * (hd / 2) * 4) +
                // decode state
                align_up(BL * 4) * 3 + align_up(BL) + align_up(max_batch * 4) * 3 +
                align_up(rows * 4) * 2 + align_up(rows) + align_up((size_t)max_batch * max_seq * 4);
@@ -207,7 +206,6 @@ extern "C" cora_status cora_model_create(const cora_model_cfg* cfg, uint64_t see
   m->logits = a.take<uint16_t>(rows * V);
   m->rope_cos = a.take<float>((size_t)m->max_seq_pad * (hd / 2));
   m->rope_sin = a.take<float>((size_t)m->max_seq_pad * (hd / 2));
-  m->tickets = a.take<int32_t>(max_batch);
   m->s_tokens = a.take<int32_t>(BL);
   m->s_prev = a.take<int32_t>(BL);
   m->s_persist = a.take<int32_t>(BL);
@@ -228,7 +226,6 @@ extern "C" cora_status cora_model_create(const cora_model_cfg* cfg, uint64_t see
   // ---- fill weights
   auto st = [&]() -> cora_status {
     HIP_TRY(hipMemsetAsync(m->weight_mem, 0, wb, s));
-    HIP_TRY(hipMemsetAsync(m->tickets, 0, max_batch * sizeof(int32_t), s));
     const double sd = cfg->init_std;
     HIP_TRY(hipMemsetAsync(m->ws_mem, 0, wsb, s));  // finite zeros in every padding region
     HIP_TRY(launch_init_bf16(m->embed, seed, 1, V, d, d, ROW_IDENTITY, 0, sd, hd, s));
@@ -457,7 +454,7 @@ static cora_status check_state(const cora_state* st, const cora_sched_cfg* sc) {
 
 static VocabGateArgs vg_args(const uint16_t* logits, int n_rows, int row_begin, int V,
                              int mask_id, const cora_state* st, int k_transfer,
-                             const cora_sched_cfg* sc, const cora_gate_cfg* gt, int32_t* tickets) {
+                             const cora_sched_cfg* sc, const cora_gate_cfg* gt) {
   VocabGateArgs a{};
   a.logits = logits; a.n_rows = n_rows; a.row_begin = row_begin; a.V = V; a.mask_id = mask_id;
   a.tokens = st->tokens; a.unresolved = st->unresolved; a.prev_top1 = st->prev_top1;
@@ -469,25 +466,17 @@ static VocabGateArgs vg_args(const uint16_t* logits, int n_rows, int row_begin, 
   a.n_blocks = st->gen_len / sc->block_len;
   a.k_transfer = k_transfer;
   a.delta_p = gt->delta_p; a.m_req = gt->m_req; a.gate_enabled = gt->gate_enabled ? 1 : 0;
-  a.tickets = tickets;
   return a;
-}
-
-extern "C" size_t cora_vocab_gate_workspace_bytes(int32_t B) {
-  return align_up((size_t)(B > 0 ? B : 0) * sizeof(int32_t));
 }
 
 extern "C" cora_status cora_vocab_gate(const uint16_t* d_logits, int32_t n_rows, int32_t row_begin,
                                        int32_t V, int32_t mask_id, cora_state* st,
                                        int32_t k_transfer, const cora_sched_cfg* sc,
-                                       const cora_gate_cfg* gt, void* d_workspace,
-                                       size_t workspace_bytes, void* hip_stream) {
+                                       const cora_gate_cfg* gt, void* hip_stream) {
   if (cora_status e = check_sched_gate(sc, gt)) return e;
   if (cora_status e = check_state(st, sc)) return e;
-  if (!d_logits || !d_workspace) return fail(CORA_ERR_INVALID_ARG, "null logits or workspace");
+  if (!d_logits) return fail(CORA_ERR_INVALID_ARG, "null logits");
   if (V < 2 || mask_id < 0 || mask_id >= V) return fail(CORA_ERR_INVALID_ARG, "bad V/mask_id");
-  if (workspace_bytes < cora_vocab_gate_workspace_bytes(st->B))
-    return fail(CORA_ERR_INVALID_ARG, "workspace too small");
   const int L = st->prompt_len + st->gen_len;
   if (row_begin >= 0) {
     if (row_begin > st->prompt_len || row_begin + n_rows < L || row_begin + n_rows > L)
@@ -497,8 +486,7 @@ extern "C" cora_status cora_vocab_gate(const uint16_t* d_logits, int32_t n_rows,
     return fail(CORA_ERR_INVALID_ARG, "block-following rows need n_rows == block_len");
   }
   if (n_rows <= 0) return fail(CORA_ERR_INVALID_ARG, "n_rows must be positive");
-  const VocabGateArgs a = vg_args(d_logits, n_rows, row_begin, V, mask_id, st, k_transfer, sc, gt,
-                                  reinterpret_cast<int32_t*>(d_workspace));
+  const VocabGateArgs a = vg_args(d_logits, n_rows, row_begin, V, mask_id, st, k_transfer, sc, gt);
   HIP_TRY(launch_vocab_gate(a, S(hip_stream)));
   return CORA_OK;
 }
@@ -510,7 +498,7 @@ static cora_status denoise_step(cora_model* m, cora_state* st, const cora_sched_
   const RowSel sel{2, L, blk, 0, st->prompt_len, blk, st->gen_len / blk, st->block_idx};
   if (cora_status e = lm_head(m, sel, B * blk, m->logits, s)) return e;
   const VocabGateArgs a = vg_args(m->logits, blk, -1, m->cfg.vocab, m->cfg.mask_id, st, -1, sc,
-                                  gt, m->tickets);
+                                  gt);
   HIP_TRY(launch_vocab_gate(a, s));
   return CORA_OK;
 }

@@ -1,21 +1,23 @@
-// Fused vocab reduction + decision rules (one launch per denoising step).
+// Vocab reduction + decision rules: two launches per denoising step.
 //
-// Phase 1, one workgroup per logits row: a single coalesced pass over the bf16 row
-// (16-byte loads) keeps a running (max, first argmax, sum of exp(l - max)) per thread,
-// merged across the wavefront with xor shuffles and across the 4 wavefronts through
-// LDS in a fixed order, so results are bitwise reproducible.  The row's top-1 token
-// is the lowest id among equal maxima, the mask id is skipped, and the confidence
-// is c = max softmax = 1 / sum_v exp(l_v - l_max) (Eq. 1).
+// k_vocab_top1, one workgroup per logits row: a single coalesced pass over the bf16 row
+// (16-byte streaming loads, the next group of four in flight while the current one is
+// consumed) keeps a running (max, sum of exp(l - max)) per thread and the chunk that first
+// reached the max, merged across the wavefront with xor shuffles and across the 4
+// wavefronts through LDS in a fixed order, so results are bitwise reproducible.  The row's
+// top-1 token is the lowest id among equal maxima, the mask id is skipped, and the
+// confidence is c = max softmax = 1 / sum_v exp(l_v - l_max) (Eq. 1).
 //
-// Phase 2, the last workgroup of each batch row to finish (a per-row ticket taken after
-// its agent-coherent result stores completed) applies, on that row's active block:
+// k_gate_rules, one workgroup per batch row, on that row's active block (the kernel
+// boundary orders it after every row's top-1 and confidence):
 //   block step 0 -> previous top-1 and counters reset (persistence is per block);
 //   Eq. (2) counter update on unresolved positions;
 //   transfer rule: the k highest-confidence unresolved positions (ties -> lower position);
 //   Eq. (3) gate on the other unresolved positions (c >= delta_p and m >= m_req);
 //   Eq. (4) commit of both sets; block done once no unresolved position is left,
 //   then the row moves to its next block.
-// The ticket counter is reset to zero by the workgroup that used it.
+// Splitting the two removes a per-row tail (agent-coherent result stores, their
+// completion, a ticket round trip) from every workgroup of the bandwidth-bound first pass.
 #include <limits.h>
 
 #include "common.hpp"
@@ -25,39 +27,58 @@ namespace cora {
 
 struct TopState {
   float m, s;
-  int arg;
+  int arg;  // during the row loop (VEC): index of the chunk that first reached m
 };
+
+constexpr float LOG2E = 1.4426950408889634f;
+
+// 2^x with the hardware v_exp_f32: results below 2^-126 flush to zero, which cannot change
+// a softmax sum that already holds the max term (1.0)
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 __device__ __forceinline__ TopState merge(TopState x, TopState y) {
   TopState r;
   r.m = fmaxf(x.m, y.m);
-  const float sx = x.m == -INFINITY ? 0.f : x.s * exp2f((x.m - r.m) * 1.4426950408889634f);
-  const float sy = y.m == -INFINITY ? 0.f : y.s * exp2f((y.m - r.m) * 1.4426950408889634f);
+  const float sx = x.m == -INFINITY ? 0.f : x.s * fast_exp2((x.m - r.m) * LOG2E);
+  const float sy = y.m == -INFINITY ? 0.f : y.s * fast_exp2((y.m - r.m) * LOG2E);
   r.s = sx + sy;
   r.arg = x.m > y.m ? x.arg : (y.m > x.m ? y.arg : min(x.arg, y.arg));
   return r;
 }
 
-__device__ __forceinline__ void consume8(TopState& t, const float (&v)[8], int idx0) {
-  float cm = v[0];
-  int ca = 0;
+// Running (max, sum of exp(l - max)) over a group of 32 logits (chunks i = 0..3 of 8): one
+// max and one rescale per group, then exp2 of every logit relative to the running max.  The
+// argmax is not tracked per element: the chunk that first raises the running max is
+// remembered (strict >, so the earliest chunk holding the maximum; the four chunk maxima
+// fall out of the max tree) and searched once after the row.
+__device__ __forceinline__ void consume32(TopState& t, const float (&v)[32], int c) {
+  float cmx[4];
 #pragma unroll
-  for (int j = 1; j < 8; ++j)
-    if (v[j] > cm) { cm = v[j]; ca = j; }
+  for (int i = 0; i < 4; ++i) {
+    float m = v[8 * i];
+#pragma unroll
+    for (int j = 1; j < 8; ++j) m = fmaxf(m, v[8 * i + j]);
+    cmx[i] = m;
+  }
+  const float cm = fmaxf(fmaxf(cmx[0], cmx[1]), fmaxf(cmx[2], cmx[3]));
   if (cm > t.m) {
-    t.s = t.m == -INFINITY ? 0.f : t.s * exp2f((t.m - cm) * 1.4426950408889634f);
+    t.s = t.m == -INFINITY ? 0.f : t.s * fast_exp2((t.m - cm) * LOG2E);
     t.m = cm;
-    t.arg = idx0 + ca;
+    t.arg = c + 256 * (cmx[0] == cm ? 0 : (cmx[1] == cm ? 1 : (cmx[2] == cm ? 2 : 3)));
   }
   if (t.m == -INFINITY) return;
-  float acc = 0.f;
+  const float ml = t.m * LOG2E;
+  float acc0 = 0.f, acc1 = 0.f;
 #pragma unroll
-  for (int j = 0; j < 8; ++j) acc += exp2f((v[j] - t.m) * 1.4426950408889634f);
-  t.s += acc;
+  for (int j = 0; j < 32; j += 2) {
+    acc0 += fast_exp2(fmaf(v[j], LOG2E, -ml));
+    acc1 += fast_exp2(fmaf(v[j + 1], LOG2E, -ml));
+  }
+  t.s += acc0 + acc1;
 }
 
 template <bool VEC>
-__global__ __launch_bounds__(256) void k_vocab_gate(VocabGateArgs a) {
+__global__ __launch_bounds__(256) void k_vocab_top1(VocabGateArgs a) {
   const int row = blockIdx.x;
   const int b = row / a.n_rows;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -65,46 +86,86 @@ __global__ __launch_bounds__(256) void k_vocab_gate(VocabGateArgs a) {
 
   TopState t{-INFINITY, 0.f, INT_MAX};
   if constexpr (VEC) {
+    // Thread tid reads chunks (16 bytes = 8 logits) tid + 256 i, in groups of 4: chunks
+    // c, c + 256, c + 512, c + 768.  The next group's loads are in flight while the current
+    // group is consumed.  Only a wavefront whose group holds the mask id's chunk (a scalar
+    // test) applies the mask override.
     const int nch = a.V >> 3;
     const int mchunk = a.mask_id >> 3, mlane = a.mask_id & 7;
+    const u32x4_t* xv = reinterpret_cast<const u32x4_t*>(x);
+    const u32x4_t NEG_INF4 = {0xff80ff80u, 0xff80ff80u, 0xff80ff80u, 0xff80ff80u};
+    auto group = [&](const u32x4_t (&w)[4], int c) {
+      float v[32];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        v[8 * i + 0] = bf16_bits_to_f32(w[i].x & 0xffff); v[8 * i + 1] = bf16_bits_to_f32(w[i].x >> 16);
+        v[8 * i + 2] = bf16_bits_to_f32(w[i].y & 0xffff); v[8 * i + 3] = bf16_bits_to_f32(w[i].y >> 16);
+        v[8 * i + 4] = bf16_bits_to_f32(w[i].z & 0xffff); v[8 * i + 5] = bf16_bits_to_f32(w[i].z >> 16);
+        v[8 * i + 6] = bf16_bits_to_f32(w[i].w & 0xffff); v[8 * i + 7] = bf16_bits_to_f32(w[i].w >> 16);
+      }
+      const int cb = __builtin_amdgcn_readfirstlane(c - lane);  // chunk of lane 0
+      const int dm = mchunk - cb;
+      if (dm >= 0 && dm < 1024 && (dm & 255) < 64) {  // this wavefront's group holds the mask id
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+            if (c + 256 * i == mchunk && j == mlane) v[8 * i + j] = -INFINITY;
+      }
+      consume32(t, v, c);
+    };
+    auto load4 = [&](u32x4_t (&w)[4], int c) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) w[i] = __builtin_nontemporal_load(xv + c + 256 * i);
+    };
     int c = tid;
-    for (; c + 256 < nch; c += 512) {  // two independent 16-byte loads in flight
-      const u32x4_t w0 = *reinterpret_cast<const u32x4_t*>(x + (int64_t)c * 8);
-      const u32x4_t w1 = *reinterpret_cast<const u32x4_t*>(x + (int64_t)(c + 256) * 8);
-      float v[8];
-      v[0] = bf16_bits_to_f32(w0.x & 0xffff); v[1] = bf16_bits_to_f32(w0.x >> 16);
-      v[2] = bf16_bits_to_f32(w0.y & 0xffff); v[3] = bf16_bits_to_f32(w0.y >> 16);
-      v[4] = bf16_bits_to_f32(w0.z & 0xffff); v[5] = bf16_bits_to_f32(w0.z >> 16);
-      v[6] = bf16_bits_to_f32(w0.w & 0xffff); v[7] = bf16_bits_to_f32(w0.w >> 16);
-      if (c == mchunk) v[mlane] = -INFINITY;
-      consume8(t, v, c * 8);
-      v[0] = bf16_bits_to_f32(w1.x & 0xffff); v[1] = bf16_bits_to_f32(w1.x >> 16);
-      v[2] = bf16_bits_to_f32(w1.y & 0xffff); v[3] = bf16_bits_to_f32(w1.y >> 16);
-      v[4] = bf16_bits_to_f32(w1.z & 0xffff); v[5] = bf16_bits_to_f32(w1.z >> 16);
-      v[6] = bf16_bits_to_f32(w1.w & 0xffff); v[7] = bf16_bits_to_f32(w1.w >> 16);
-      if (c + 256 == mchunk) v[mlane] = -INFINITY;
-      consume8(t, v, (c + 256) * 8);
+    if (c + 768 < nch) {
+      // two register groups used alternately (no copies): one in flight, one consumed
+      u32x4_t ga[4], gb[4];
+      load4(ga, c);
+      while (true) {
+        if (c + 1024 + 768 >= nch) { group(ga, c); c += 1024; break; }
+        load4(gb, c + 1024);
+        group(ga, c);
+        c += 1024;
+        if (c + 1024 + 768 >= nch) { group(gb, c); c += 1024; break; }
+        load4(ga, c + 1024);
+        group(gb, c);
+        c += 1024;
+      }
     }
-    for (; c < nch; c += 256) {
-      const u32x4_t w0 = *reinterpret_cast<const u32x4_t*>(x + (int64_t)c * 8);
-      float v[8];
-      v[0] = bf16_bits_to_f32(w0.x & 0xffff); v[1] = bf16_bits_to_f32(w0.x >> 16);
-      v[2] = bf16_bits_to_f32(w0.y & 0xffff); v[3] = bf16_bits_to_f32(w0.y >> 16);
-      v[4] = bf16_bits_to_f32(w0.z & 0xffff); v[5] = bf16_bits_to_f32(w0.z >> 16);
-      v[6] = bf16_bits_to_f32(w0.w & 0xffff); v[7] = bf16_bits_to_f32(w0.w >> 16);
-      if (c == mchunk) v[mlane] = -INFINITY;
-      consume8(t, v, c * 8);
+    if (c < nch) {  // at most 3 chunks left: one guarded group, missing chunks -inf
+      u32x4_t w[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) w[i] = c + 256 * i < nch ? xv[c + 256 * i] : NEG_INF4;
+      group(w, c);
+    }
+    // lowest index holding the max inside the remembered chunk (mask id excluded)
+    if (t.m == -INFINITY) {
+      t.arg = INT_MAX;
+    } else {
+      const int ch = t.arg;
+      const u32x4_t w = xv[ch];
+      const uint32_t wd[4] = {w.x, w.y, w.z, w.w};
+      int found = INT_MAX;
+#pragma unroll
+      for (int e = 7; e >= 0; --e) {
+        const float f = bf16_bits_to_f32((e & 1) ? (wd[e >> 1] >> 16) : (wd[e >> 1] & 0xffff));
+        if (f == t.m && !(ch == mchunk && e == mlane)) found = ch * 8 + e;
+      }
+      t.arg = found;
     }
   } else {
     for (int v = tid; v < a.V; v += 256) {
       if (v == a.mask_id) continue;
       const float f = bf16_bits_to_f32(x[v]);
+      if (f == -INFINITY) continue;
       if (f > t.m) {
-        t.s = t.m == -INFINITY ? 0.f : t.s * exp2f((t.m - f) * 1.4426950408889634f);
+        t.s = t.m == -INFINITY ? 0.f : t.s * fast_exp2((t.m - f) * LOG2E);
         t.m = f;
         t.arg = v;
       }
-      t.s += exp2f((f - t.m) * 1.4426950408889634f);
+      t.s += fast_exp2((f - t.m) * LOG2E);
     }
   }
 #pragma unroll
@@ -117,29 +178,21 @@ __global__ __launch_bounds__(256) void k_vocab_gate(VocabGateArgs a) {
   }
   __shared__ float sm_m[4], sm_s[4];
   __shared__ int sm_a[4];
-  __shared__ int is_last;
   if (lane == 0) { sm_m[wave] = t.m; sm_s[wave] = t.s; sm_a[wave] = t.arg; }
   __syncthreads();
   if (tid == 0) {
     TopState r{sm_m[0], sm_s[0], sm_a[0]};
     for (int w = 1; w < 4; ++w) r = merge(r, TopState{sm_m[w], sm_s[w], sm_a[w]});
-    // agent-coherent (sc1) stores instead of a release fence, which would write back the
-    // whole L2: once they complete (vmcnt 0) they are visible to the last workgroup
-    __hip_atomic_store(&a.top1[row], r.arg, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __hip_atomic_store(&a.conf[row], 1.0f / r.s, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __builtin_amdgcn_s_waitcnt(0);
-    const int old =
-        __hip_atomic_fetch_add(&a.tickets[b], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    is_last = (old == a.n_rows - 1);
+    a.top1[row] = r.arg;
+    a.conf[row] = 1.0f / r.s;
   }
-  __syncthreads();
-  if (!is_last) return;
+}
 
-  // ---- phase 2: decision rules for batch row b --------------------------------------
+__global__ __launch_bounds__(256) void k_gate_rules(VocabGateArgs a) {
+  const int b = blockIdx.x, tid = threadIdx.x;
   const int BL = a.block_len;
   const int blk = a.block_idx[b];
   const int s = a.step_idx[b];
-  if (tid == 0) __hip_atomic_store(&a.tickets[b], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   if (blk < 0 || s < 0) {  // malformed state: touch nothing outside the scored rows
     if (tid == 0) a.done[b] = 0;
     return;
@@ -161,8 +214,8 @@ __global__ __launch_bounds__(256) void k_vocab_gate(VocabGateArgs a) {
   if (act) {
     U = a.unresolved[gi];
     const int64_t ri = (int64_t)b * a.n_rows + (lo + tid - row0);
-    xh = __hip_atomic_load(&a.top1[ri], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    c = __hip_atomic_load(&a.conf[ri], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    xh = a.top1[ri];
+    c = a.conf[ri];
     int prev = s == 0 ? -1 : a.prev_top1[gi];
     int mm = s == 0 ? 0 : a.persist[gi];
     if (U) {                                              // Eq. (2)
@@ -206,10 +259,14 @@ __global__ __launch_bounds__(256) void k_vocab_gate(VocabGateArgs a) {
 hipError_t launch_vocab_gate(const VocabGateArgs& a, hipStream_t s) {
   const int rows = a.B * a.n_rows;
   if (rows == 0) return hipSuccess;
+  if (a.block_len > 256) return hipErrorInvalidValue;  // k_gate_rules: one thread per position
   if (a.V % 8 == 0)
-    hipLaunchKernelGGL(k_vocab_gate<true>, dim3(rows), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(k_vocab_top1<true>, dim3(rows), dim3(256), 0, s, a);
   else
-    hipLaunchKernelGGL(k_vocab_gate<false>, dim3(rows), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(k_vocab_top1<false>, dim3(rows), dim3(256), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_gate_rules, dim3(a.B), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

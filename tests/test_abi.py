@@ -82,11 +82,10 @@ def test_vocab_gate_rejects_bad_arguments():
     sc, gt = L.SchedCfg(32, 16), L.GateCfg(0.65, 1, 1, 0)
     st = L.State()
     assert lib.cora_vocab_gate(None, 32, -1, 100, 5, ctypes.byref(st), -1, ctypes.byref(sc),
-                               ctypes.byref(gt), None, 0, None) == -1
+                               ctypes.byref(gt), None) == -1
     bad_sched = L.SchedCfg(512, 16)
     assert lib.cora_vocab_gate(None, 32, -1, 100, 5, ctypes.byref(st), -1,
-                               ctypes.byref(bad_sched), ctypes.byref(gt), None, 0, None) == -2
+                               ctypes.byref(bad_sched), ctypes.byref(gt), None) == -2
     bad_gate = L.GateCfg(0.65, 1, 1, 1)
     assert lib.cora_vocab_gate(None, 32, -1, 100, 5, ctypes.byref(st), -1, ctypes.byref(sc),
-                               ctypes.byref(bad_gate), None, 0, None) == -2
-    assert lib.cora_vocab_gate_workspace_bytes(8) >= 32
+                               ctypes.byref(bad_gate), None) == -2
