@@ -3,10 +3,11 @@
 // k_vocab_top1, one workgroup per logits row: a single coalesced pass over the bf16 row
 // (16-byte streaming loads, the next group of four in flight while the current one is
 // consumed) keeps a running (max, sum of exp(l - max)) per thread and the chunk that first
-// reached the max, merged across the wavefront with xor shuffles and across the 4
-// wavefronts through LDS in a fixed order, so results are bitwise reproducible.  The row's
-// top-1 token is the lowest id among equal maxima, the mask id is skipped, and the
-// confidence is c = max softmax = 1 / sum_v exp(l_v - l_max) (Eq. 1).
+// reached the max (its raw words kept in registers), merged across the wavefront with xor
+// shuffles and across the 4 wavefronts through LDS in a fixed order, so results are
+// bitwise reproducible.  The row's top-1 token is the lowest id among equal maxima, the
+// mask id is skipped, and the confidence is c = max softmax = 1 / sum_v exp(l_v - l_max)
+// (Eq. 1).
 //
 // k_gate_rules, one workgroup per batch row, on that row's active block (the kernel
 // boundary orders it after every row's top-1 and confidence):
@@ -29,6 +30,10 @@ struct TopState {
   float m, s;
   int arg;  // during the row loop (VEC): index of the chunk that first reached m
 };
+// raw words of the chunk that first reached the running max (VEC row loop)
+struct BestChunk {
+  uint32_t w0, w1, w2, w3;
+};
 
 constexpr float LOG2E = 1.4426950408889634f;
 
@@ -49,9 +54,10 @@ __device__ __forceinline__ TopState merge(TopState x, TopState y) {
 // Running (max, sum of exp(l - max)) over a group of 32 logits (chunks i = 0..3 of 8): one
 // max and one rescale per group, then exp2 of every logit relative to the running max.  The
 // argmax is not tracked per element: the chunk that first raises the running max is
-// remembered (strict >, so the earliest chunk holding the maximum; the four chunk maxima
-// fall out of the max tree) and searched once after the row.
-__device__ __forceinline__ void consume32(TopState& t, const float (&v)[32], int c) {
+// remembered with its raw words (strict >, so the earliest chunk holding the maximum; the
+// four chunk maxima fall out of the max tree) and searched once after the row.
+__device__ __forceinline__ void consume32(TopState& t, BestChunk& best, const float (&v)[32],
+                                          const u32x4_t (&w)[4], int c) {
   float cmx[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -64,7 +70,10 @@ __device__ __forceinline__ void consume32(TopState& t, const float (&v)[32], int
   if (cm > t.m) {
     t.s = t.m == -INFINITY ? 0.f : t.s * fast_exp2((t.m - cm) * LOG2E);
     t.m = cm;
-    t.arg = c + 256 * (cmx[0] == cm ? 0 : (cmx[1] == cm ? 1 : (cmx[2] == cm ? 2 : 3)));
+    const int i = cmx[0] == cm ? 0 : (cmx[1] == cm ? 1 : (cmx[2] == cm ? 2 : 3));
+    const u32x4_t bw = i == 0 ? w[0] : (i == 1 ? w[1] : (i == 2 ? w[2] : w[3]));
+    best = BestChunk{bw.x, bw.y, bw.z, bw.w};
+    t.arg = c + 256 * i;
   }
   if (t.m == -INFINITY) return;
   const float ml = t.m * LOG2E;
@@ -94,6 +103,7 @@ __global__ __launch_bounds__(256) void k_vocab_top1(VocabGateArgs a) {
     const int mchunk = a.mask_id >> 3, mlane = a.mask_id & 7;
     const u32x4_t* xv = reinterpret_cast<const u32x4_t*>(x);
     const u32x4_t NEG_INF4 = {0xff80ff80u, 0xff80ff80u, 0xff80ff80u, 0xff80ff80u};
+    BestChunk best{0u, 0u, 0u, 0u};
     auto group = [&](const u32x4_t (&w)[4], int c) {
       float v[32];
 #pragma unroll
@@ -112,7 +122,7 @@ __global__ __launch_bounds__(256) void k_vocab_top1(VocabGateArgs a) {
           for (int j = 0; j < 8; ++j)
             if (c + 256 * i == mchunk && j == mlane) v[8 * i + j] = -INFINITY;
       }
-      consume32(t, v, c);
+      consume32(t, best, v, w, c);
     };
     auto load4 = [&](u32x4_t (&w)[4], int c) {
 #pragma unroll
@@ -145,8 +155,7 @@ __global__ __launch_bounds__(256) void k_vocab_top1(VocabGateArgs a) {
       t.arg = INT_MAX;
     } else {
       const int ch = t.arg;
-      const u32x4_t w = xv[ch];
-      const uint32_t wd[4] = {w.x, w.y, w.z, w.w};
+      const uint32_t wd[4] = {best.w0, best.w1, best.w2, best.w3};
       int found = INT_MAX;
 #pragma unroll
       for (int e = 7; e >= 0; --e) {
