@@ -33,8 +33,8 @@ DELTA_P, M_REQ = 0.65, 1
 # plain 1 GiB copy (profiles/gate_up_gemm_llada8b_gen256.md, profiles/vocab_gate_8x512x126464.md).
 # Valid only for the kernel source the counters were taken on.
 COUNTER_TRAFFIC = {
-    "gate_up": ("paper_2608_11235_amd/csrc/gemm.hip", "bfb20c85ff602a87", 247642726),
-    "vocab_gate": ("paper_2608_11235_amd/csrc/vocab_gate.hip", "ba73da83ca2a6a22", 1036616704),
+    "gate_up": ("paper_2608_11235_amd/csrc/gemm.hip", "6dd886b32a1882aa", 247652984),
+    "vocab_gate": ("paper_2608_11235_amd/csrc/vocab_gate.hip", "7d2ce1844c851bce", 1036512864),
 }
 
 

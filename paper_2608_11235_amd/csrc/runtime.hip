@@ -280,12 +280,26 @@ extern "C" cora_status cora_model_device_bytes(cora_model* m, size_t* wbytes, si
 }
 
 // ---- timing ------------------------------------------------------------------------------
+// Timing events record without a system-scope fence: a measurement event must not add an
+// L2 writeback / invalidate around the kernel it brackets.
+static cora_status grow_events(cora_model* m, size_t n) {
+  while (m->ev.size() < n) {
+    hipEvent_t e;
+    HIP_TRY(hipEventCreateWithFlags(&e, hipEventDisableSystemFence));
+    m->ev.push_back(e);
+  }
+  return CORA_OK;
+}
+
 extern "C" cora_status cora_model_set_timing(cora_model* m, int32_t enable) {
   if (!m) return fail(CORA_ERR_INVALID_ARG, "null model");
   m->timing = enable != 0;
   m->ev_used = 0;
   m->acc_ms = 0.0;
   m->launches = 0;
+  // created up front so the timed passes do not pay for them
+  if (m->timing)
+    if (cora_status st = grow_events(m, 2 * m->layers.size() * 64)) return st;
   return CORA_OK;
 }
 
@@ -314,11 +328,7 @@ static cora_status timed_event(cora_model* m, hipStream_t s) {
     if (m->ev.size() >= 8192) {
       if (cora_status st = drain_events(m)) return st;
     } else {
-      for (int i = 0; i < 64; ++i) {
-        hipEvent_t e;
-        HIP_TRY(hipEventCreate(&e));
-        m->ev.push_back(e);
-      }
+      if (cora_status st = grow_events(m, m->ev.size() + 64)) return st;
     }
   }
   HIP_TRY(hipEventRecord(m->ev[m->ev_used++], s));
