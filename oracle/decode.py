@@ -19,8 +19,12 @@ Readings of points the paper leaves open (the R-numbers of the design doc):
         active block; equal confidence -> lower position first.
     R3  candidates are U restricted to the active block.
     R4  order in a step: scores -> counter update -> T -> A on (U \\ T) -> commit -> terminate.
-    R5  BLOCK persistence scope: counters and previous top-1 reset when a block
-        becomes active (first executed step of the block).
+    R5  persistence scope.  BLOCK (default): counters and previous top-1 reset when a
+        block becomes active (its first executed step), so only the active block is
+        scored.  GLOBAL: every unresolved generation position is scored on every
+        executed pass and its counter runs across blocks without a reset; transfer and
+        gate still act on the active block only, so a block whose positions already
+        persisted during earlier blocks can end after one pass.
     R7  both gate comparisons inclusive; the confidence test and the transfer
         ranking are taken on c rounded to fp32, against fp32(delta_p).
     R9  argmax ties -> lowest token id.  R10  the mask id is never predicted.
@@ -84,12 +88,13 @@ def gate_accept(c32, m, delta_p, m_req):
 
 # --- one denoising step on one batch row ---------------------------------------------------
 def step_row(st, b, logits_blk, prompt_len, block_len, steps_per_block, n_blocks, mask_id,
-             delta_p, m_req, gate_enabled, k_override=None, logits_row0=None):
+             delta_p, m_req, gate_enabled, k_override=None, logits_row0=None, scope="block"):
     """Apply the decision part of one executed step to batch row b, in place.
 
     logits_blk [n_rows, V] are the logits of canvas rows starting at `logits_row0`
-    (default: the active block's first position).  Returns a dict with x_hat, c, c32
-    for those rows, and T, A, done for the block."""
+    (default: the active block's first position).  scope "block" or "global" (R5); the
+    global scope needs rows covering every unresolved position.  Returns a dict with
+    x_hat, c, c32 for those rows, and T, A, done for the block."""
     blk = int(st["block_idx"][b])
     if blk >= n_blocks:                       # row already finished all blocks
         return {"finished": True, "T": np.zeros(0, np.int64), "A": np.zeros(0, np.int64),
@@ -97,23 +102,30 @@ def step_row(st, b, logits_blk, prompt_len, block_len, steps_per_block, n_blocks
     lo = prompt_len + blk * block_len
     pos = np.arange(lo, lo + block_len)
     s = int(st["step_idx"][b])
-    if s == 0:                                # R5: the block becomes active
+    if scope == "block" and s == 0:           # R5: the block becomes active
         st["prev_top1"][b, pos] = NONE
         st["persist"][b, pos] = 0
 
     row0 = lo if logits_row0 is None else logits_row0
     x_hat_rows, c_rows = top1_confidence(logits_blk, mask_id)              # Eq. (1)
+    scored = np.arange(row0, row0 + len(x_hat_rows))
     x_hat = np.full(st["tokens"].shape[1], NONE, dtype=np.int64)
     c = np.zeros(st["tokens"].shape[1], dtype=np.float64)
-    x_hat[pos] = x_hat_rows[pos - row0]
-    c[pos] = c_rows[pos - row0]
+    x_hat[scored] = x_hat_rows
+    c[scored] = c_rows
     c32 = c.astype(np.float32)
 
     U_blk = pos[st["unresolved"][b, pos] == 1]                             # R3
-    new_prev, new_m = persistence_update(st["prev_top1"][b, U_blk],       # Eq. (2)
-                                         st["persist"][b, U_blk], x_hat[U_blk])
-    st["prev_top1"][b, U_blk] = new_prev
-    st["persist"][b, U_blk] = new_m
+    if scope == "global":                     # R5: every scored unresolved position
+        U_upd = scored[st["unresolved"][b, scored] == 1]
+        unscored = np.setdiff1d(np.nonzero(st["unresolved"][b])[0], scored)
+        assert len(unscored) == 0, "global scope needs scores for every unresolved position"
+    else:
+        U_upd = U_blk
+    new_prev, new_m = persistence_update(st["prev_top1"][b, U_upd],       # Eq. (2)
+                                         st["persist"][b, U_upd], x_hat[U_upd])
+    st["prev_top1"][b, U_upd] = new_prev
+    st["persist"][b, U_upd] = new_m
 
     M = block_len                              # R1: the block starts fully masked
     k = transfer_schedule(M, steps_per_block)[s] if k_override is None else k_override
@@ -150,12 +162,14 @@ def copy_state(st):
 
 # --- the gated block decode (Fig. 2; Section 3, "From acceptance to runtime") -----------
 def block_decode(logits_fn, prompt, gen_len, mask_id, block_len, steps_per_block,
-                 delta_p, m_req, gate_enabled, record=False):
+                 delta_p, m_req, gate_enabled, record=False, scope="block"):
     """Decode every batch row independently (R15), block by block, left to right.
 
     logits_fn(tokens [B, L], rows list-of-arrays) -> list of [len(rows_b), V] logits.
     Each executed step runs one dense pass, then the decision rules; a block ends
-    once it holds no unresolved position, skipping its remaining passes.
+    once it holds no unresolved position, skipping its remaining passes.  The block
+    scope scores the active block's rows, the global scope the whole generation
+    region (R5).
 
     Returns (tokens [B, L], passes [B, n_blocks], trace) where trace holds the
     pre-step state and step outputs of every executed pass when record=True."""
@@ -177,14 +191,18 @@ def block_decode(logits_fn, prompt, gen_len, mask_id, block_len, steps_per_block
     trace = []
     while (st["block_idx"] < n_blocks).any():
         active = [b for b in range(B) if st["block_idx"][b] < n_blocks]
-        rows = [block_positions(st, b, P, block_len, n_blocks) for b in range(B)]
+        if scope == "global":
+            rows = [np.arange(P, L) for _ in range(B)]
+        else:
+            rows = [block_positions(st, b, P, block_len, n_blocks) for b in range(B)]
         pre = copy_state(st) if record else None
         logits = logits_fn(st["tokens"].copy(), rows)
         outs = {}
         for b in active:
             blk = int(st["block_idx"][b])
             outs[b] = step_row(st, b, logits[b], P, block_len, steps_per_block, n_blocks,
-                               mask_id, delta_p, m_req, gate_enabled)
+                               mask_id, delta_p, m_req, gate_enabled,
+                               logits_row0=int(rows[b][0]), scope=scope)
             passes[b, blk] += 1
         if record:
             trace.append({"pre": pre, "rows": rows, "logits": logits, "out": outs})

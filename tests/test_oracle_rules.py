@@ -106,16 +106,18 @@ class _RandomModel:
         return out
 
 
+@pytest.mark.parametrize("scope", ["block", "global"])
 @pytest.mark.parametrize("seed", range(6))
 @pytest.mark.parametrize("delta_p,m_req,gate", [(0.65, 1, True), (0.3, 0, True), (0.5, 2, True),
-                                                 (0.65, 1, False)])
-def test_decode_invariants(seed, delta_p, m_req, gate):
+                                                 (0.0, 1, True), (0.65, 1, False)])
+def test_decode_invariants(seed, delta_p, m_req, gate, scope):
+    """(0.0, 1) is the persistence-only variant, (0.3, 0) confidence-only, m = 2 two checks."""
     V, P, G, blk, S = 23, 5, 24, 8, 4
     mask_id = V - 1
     model = _RandomModel(V, P + G, seed, scale=1.5)
     prompt = np.random.default_rng(100 + seed).integers(0, V - 1, (2, P))
     tokens, passes, trace = decode.block_decode(model, prompt, G, mask_id, blk, S, delta_p,
-                                                m_req, gate, record=True)
+                                                m_req, gate, record=True, scope=scope)
     ks = decode.transfer_schedule(blk, S)
     for step in trace:
         pre = step["pre"]
@@ -127,14 +129,15 @@ def test_decode_invariants(seed, delta_p, m_req, gate):
             assert len(np.intersect1d(T, A)) == 0                  # gate only on U \ T
             assert set(T) <= set(U_blk) and set(A) <= set(U_blk)   # only the active block
             assert len(T) == min(ks[out["step"]], len(U_blk))      # exactly k_s fixed
+            row0 = lo if scope == "block" else P
             for i in A:                                            # Eq. (3)
-                assert out["c32"][i - lo] >= np.float32(delta_p) and out["m"][i] >= m_req
+                assert out["c32"][i - row0] >= np.float32(delta_p) and out["m"][i] >= m_req
             if not gate:
                 assert len(A) == 0
             # T holds the highest confidences of U_blk
             if len(T) and len(U_blk) > len(T):
                 rest = np.setdiff1d(U_blk, T)
-                assert out["c32"][T - lo].min() >= out["c32"][rest - lo].max()
+                assert out["c32"][T - row0].min() >= out["c32"][rest - row0].max()
     # Eq. (4): U shrinks by exactly T and A, committed tokens never change afterwards
     for s0, s1 in zip(trace[:-1], trace[1:]):
         for b, out in s0["out"].items():
@@ -147,8 +150,10 @@ def test_decode_invariants(seed, delta_p, m_req, gate):
     assert (tokens != mask_id).all()
     if not gate:
         assert (passes == S).all()                                   # dense horizon
-    elif m_req >= 1:
+    elif m_req >= 1 and scope == "block":
         assert (passes >= min(m_req + 1, S)).all()                   # persistence needs repeats
+    elif m_req >= 1:
+        assert (passes[:, 0] >= min(m_req + 1, S)).all()             # first block: no history
     assert 0.0 <= theory.step_ratio(passes, np.full_like(passes, S)) <= 1.0
 
 
@@ -182,3 +187,65 @@ def test_batch_rows_are_independent():
     for b in range(3):
         t1, p1, _ = decode.block_decode(model, prompt[b:b + 1], G, V - 1, blk, S, 0.4, 1, True)
         assert (t1[0] == t_all[b]).all() and (p1[0] == p_all[b]).all()
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_global_scope_gate_off_is_dense(seed):
+    """R5 only changes what the gate sees: with the gate off both scopes are the original
+    decoder (dense endpoint, S passes per block)."""
+    V, P, G, blk, S = 19, 4, 16, 8, 8
+    model = _RandomModel(V, P + G, seed, scale=3.0)
+    prompt = np.random.default_rng(seed).integers(0, V - 1, (1, P))
+    t_g, p_g, _ = decode.block_decode(model, prompt, G, V - 1, blk, S, 0.65, 1, False,
+                                      scope="global")
+    t_end, p_end = decode.dense_endpoint(model, prompt, G, V - 1, blk, S)
+    assert (t_g == t_end).all() and (p_g == p_end).all()
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_global_counters_dominate_block(seed):
+    """On one trajectory (gate off, so both scopes decode identically) the GLOBAL counter of
+    an active-block position is never below its BLOCK counter: BLOCK restarts it at the
+    block's first executed step, GLOBAL has counted since the position's first pass."""
+    V, P, G, blk, S = 13, 3, 24, 8, 4
+    model = _RandomModel(V, P + G, seed, scale=0.7)
+    prompt = np.random.default_rng(seed).integers(0, V - 1, (1, P))
+    _, _, tr_b = decode.block_decode(model, prompt, G, V - 1, blk, S, 0.65, 1, False,
+                                     record=True, scope="block")
+    _, _, tr_g = decode.block_decode(model, prompt, G, V - 1, blk, S, 0.65, 1, False,
+                                     record=True, scope="global")
+    assert len(tr_b) == len(tr_g)
+    strictly = 0
+    for sb, sg in zip(tr_b, tr_g):
+        ob, og = sb["out"][0], sg["out"][0]
+        lo = P + ob["block"] * blk
+        pos = np.arange(lo, lo + blk)
+        U = pos[sb["pre"]["unresolved"][0, pos] == 1]
+        assert (og["m"][U] >= ob["m"][U]).all()
+        strictly += int((og["m"][U] > ob["m"][U]).sum())
+    assert strictly > 0   # later blocks did inherit history
+
+
+def test_global_scope_worked_example():
+    """Hand-worked (R5): V = 3 (tokens 0, 1; mask 2), prompt 1, gen 4, blocks of 2, S = 2
+    (k_s = 1, 1), delta_p 0.6, m = 1.  Every position's logits are (4, 0, -) on every pass:
+    top-1 token 0 with c = e^4 / (e^4 + 1) = 0.982, equal confidences -> lower position.
+      BLOCK: each block starts with fresh counters: pass 1 fixes its first position by the
+      transfer rule (the other has m = 0), pass 2 transfers the second -> passes (2, 2).
+      GLOBAL: positions 3, 4 are scored from pass 1: after passes 1-2 their counters are 1;
+      pass 3 (block 1, m = 2) transfers 3 and the gate accepts 4 -> passes (2, 1)."""
+    V, mask = 3, 2
+
+    def fn(tokens, rows):
+        return [np.tile(np.array([4.0, 0.0, 0.0]), (len(r), 1)) for r in rows]
+
+    prompt = np.array([[1]])
+    t_b, p_b, tr_b = decode.block_decode(fn, prompt, 4, mask, 2, 2, 0.6, 1, True, record=True,
+                                         scope="block")
+    t_g, p_g, tr_g = decode.block_decode(fn, prompt, 4, mask, 2, 2, 0.6, 1, True, record=True,
+                                         scope="global")
+    assert p_b.tolist() == [[2, 2]] and p_g.tolist() == [[2, 1]]
+    assert t_b.tolist() == [[1, 0, 0, 0, 0]] and t_g.tolist() == [[1, 0, 0, 0, 0]]
+    assert [o["out"][0]["T"].tolist() for o in tr_g] == [[1], [2], [3]]
+    assert [o["out"][0]["A"].tolist() for o in tr_g] == [[], [], [4]]
+    assert tr_g[2]["out"][0]["m"][4] == 2 and tr_b[3]["out"][0]["m"][4] == 1
