@@ -74,8 +74,14 @@ typedef struct {
 /* Residual gate of Eq. (3): accept i iff c_i >= delta_p and m_i >= m_req,
  * both inclusive, on unresolved active-block positions the transfer rule did
  * not fix.  gate_enabled = 0 gives the original dense decoder (no position
- * accepted).  persist_scope: 0 = BLOCK (counters reset when a block becomes
- * active; the only scope implemented, others return CORA_ERR_UNSUPPORTED). */
+ * accepted).  persist_scope (the counter of Eq. (2) in blockwise decoding):
+ * 0 = BLOCK: previous top-1 and counters reset when a block becomes active
+ * (its first executed step), only the active block is scored;
+ * 1 = GLOBAL: every unresolved generation position is scored on every
+ * executed pass and its counter runs across blocks without a reset, so a
+ * block whose positions already persisted can end after one pass; transfer
+ * and gate still act on the active block only.  Other values return
+ * CORA_ERR_UNSUPPORTED. */
 typedef struct {
   float delta_p;
   int32_t m_req, gate_enabled, persist_scope;
@@ -138,8 +144,10 @@ cora_status cora_forward_logits(cora_model *model, const int32_t *d_tokens, int3
 
 /* One executed denoising step on every row of `state` that is still decoding:
  * dense pass, LM head on the active block rows of each batch row, then the
- * vocab/gate kernel (Eq. 1, Eq. 2, transfer rule, Eq. 3, Eq. 4, termination;
- * see cora_vocab_gate).  top1/conf are [B, block_len].  Asynchronous. */
+ * vocab/gate kernels (Eq. 1, Eq. 2, transfer rule, Eq. 3, Eq. 4, termination;
+ * see cora_vocab_gate).  top1/conf are [B, block_len] (the active block's
+ * rows) under the BLOCK scope and [B, gen_len] (the generation region, LM head
+ * and row reduction in chunks of up to 256 rows) under GLOBAL.  Asynchronous. */
 cora_status cora_denoise_step(cora_model *model, cora_state *state, const cora_sched_cfg *sched,
                               const cora_gate_cfg *gate, void *hip_stream);
 
@@ -153,9 +161,11 @@ cora_status cora_denoise_step(cora_model *model, cora_state *state, const cora_s
  * k highest-confidence unresolved positions (ties: lower position) fixed
  * (k = k_transfer if >= 0, else the schedule's k_s), the gate on the rest,
  * commit of both sets, and the block/step advance once the block is empty.
- * A fixed row_begin must cover the whole generation region.  Two kernel
- * launches on hip_stream (row reduction, then the decision rules); calls on one
- * state must not overlap.  Asynchronous. */
+ * A fixed row_begin must cover the whole generation region; the GLOBAL
+ * persistence scope needs fixed rows (it updates every scored unresolved
+ * position).  top1/conf receive [B, n_rows].  Two kernel launches on
+ * hip_stream (row reduction, then the decision rules); calls on one state must
+ * not overlap.  Asynchronous. */
 cora_status cora_vocab_gate(const uint16_t *d_logits, int32_t n_rows, int32_t row_begin,
                             int32_t V, int32_t mask_id, cora_state *state, int32_t k_transfer,
                             const cora_sched_cfg *sched, const cora_gate_cfg *gate,

@@ -88,6 +88,10 @@ hipError_t launch_attention(const uint16_t* q, const uint16_t* k, const uint16_t
                             int num_cus, hipStream_t s);
 
 // ---- vocab / gate (K9) -------------------------------------------------------------------
+// Logits rows r of batch row b (row-major [B, n_rows, V]) score canvas position
+// row_begin + r (row_begin >= 0) or lo_b + r (row_begin < 0, lo_b = active block start).
+// Their top-1 / confidence go to top1/conf[b * out_ld + out_off + r], so a region can be
+// scored in chunks into one [B, out_ld] array.
 struct VocabGateArgs {
   const uint16_t* logits; int n_rows; int row_begin; int V; int mask_id;
   int32_t* tokens; uint8_t* unresolved; int32_t* prev_top1; int32_t* persist;
@@ -96,7 +100,13 @@ struct VocabGateArgs {
   int B, L, prompt_len, block_len, steps_per_block, n_blocks;
   int k_transfer;  // >= 0 fixed k, < 0: schedule
   float delta_p; int m_req; int gate_enabled;
+  int persist_scope;  // 0 BLOCK, 1 GLOBAL (every scored unresolved position, no block reset)
+  int out_ld, out_off;
 };
-hipError_t launch_vocab_gate(const VocabGateArgs& a, hipStream_t s);
+// top-1 and confidence of every logits row
+hipError_t launch_vocab_top1(const VocabGateArgs& a, hipStream_t s);
+// decision rules per batch row, reading the scores of rows [row_begin, row_begin + n_rows)
+// (n_rows == out_ld) or of the active block (row_begin < 0)
+hipError_t launch_gate_rules(const VocabGateArgs& a, hipStream_t s);
 
 }  // namespace cora

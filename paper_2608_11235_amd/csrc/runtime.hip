@@ -165,7 +165,7 @@ extern "C" cora_status cora_model_create(const cora_model_cfg* cfg, uint64_t see
                2 * align_up((size_t)m->max_seq_pad * (hd / 2) * 4) +
                // decode state
                align_up(BL * 4) * 3 + align_up(BL) + align_up(max_batch * 4) * 3 +
-               align_up(rows * 4) * 2 + align_up(rows) + align_up((size_t)max_batch * max_seq * 4);
+               align_up(BL * 4) * 2 + align_up(rows) + align_up((size_t)max_batch * max_seq * 4);
   hipError_t e = hipMalloc(&m->weight_mem, wb);
   if (e != hipSuccess) {
     cora_model_destroy(m);
@@ -213,8 +213,8 @@ extern "C" cora_status cora_model_create(const cora_model_cfg* cfg, uint64_t see
   m->s_block = a.take<int32_t>(max_batch);
   m->s_step = a.take<int32_t>(max_batch);
   m->s_done = a.take<int32_t>(max_batch);
-  m->s_top1 = a.take<int32_t>(rows);
-  m->s_conf = a.take<float>(rows);
+  m->s_top1 = a.take<int32_t>(BL);   // [B, gen_len] under the GLOBAL scope
+  m->s_conf = a.take<float>(BL);
   m->s_decision = a.take<uint8_t>(rows);
   m->s_passes = a.take<int32_t>((size_t)max_batch * max_seq);
   e = hipHostMalloc((void**)&m->h_block, max_batch * sizeof(int32_t), hipHostMallocDefault);
@@ -444,8 +444,8 @@ static cora_status check_sched_gate(const cora_sched_cfg* sc, const cora_gate_cf
     return fail(CORA_ERR_UNSUPPORTED, "block_len must lie in [1, 256]");
   if (sc->steps_per_block < 1 || sc->steps_per_block > sc->block_len)
     return fail(CORA_ERR_INVALID_ARG, "steps_per_block must lie in [1, block_len]");
-  if (gt->persist_scope != 0)
-    return fail(CORA_ERR_UNSUPPORTED, "only the BLOCK persistence scope is implemented");
+  if (gt->persist_scope != 0 && gt->persist_scope != 1)
+    return fail(CORA_ERR_UNSUPPORTED, "persist_scope must be 0 (BLOCK) or 1 (GLOBAL)");
   if (gt->m_req < 0 || isnan(gt->delta_p))
     return fail(CORA_ERR_INVALID_ARG, "m_req must be >= 0 and delta_p a number");
   return CORA_OK;
@@ -476,6 +476,9 @@ static VocabGateArgs vg_args(const uint16_t* logits, int n_rows, int row_begin, 
   a.n_blocks = st->gen_len / sc->block_len;
   a.k_transfer = k_transfer;
   a.delta_p = gt->delta_p; a.m_req = gt->m_req; a.gate_enabled = gt->gate_enabled ? 1 : 0;
+  a.persist_scope = gt->persist_scope;
+  a.out_ld = n_rows;
+  a.out_off = 0;
   return a;
 }
 
@@ -494,10 +497,14 @@ extern "C" cora_status cora_vocab_gate(const uint16_t* d_logits, int32_t n_rows,
                                         "inside the canvas");
   } else if (n_rows != sc->block_len) {
     return fail(CORA_ERR_INVALID_ARG, "block-following rows need n_rows == block_len");
+  } else if (gt->persist_scope == 1) {
+    return fail(CORA_ERR_INVALID_ARG, "the GLOBAL persistence scope needs fixed rows covering "
+                                      "the generation region");
   }
   if (n_rows <= 0) return fail(CORA_ERR_INVALID_ARG, "n_rows must be positive");
   const VocabGateArgs a = vg_args(d_logits, n_rows, row_begin, V, mask_id, st, k_transfer, sc, gt);
-  HIP_TRY(launch_vocab_gate(a, S(hip_stream)));
+  HIP_TRY(launch_vocab_top1(a, S(hip_stream)));
+  HIP_TRY(launch_gate_rules(a, S(hip_stream)));
   return CORA_OK;
 }
 
@@ -505,11 +512,30 @@ static cora_status denoise_step(cora_model* m, cora_state* st, const cora_sched_
                                 const cora_gate_cfg* gt, hipStream_t s) {
   const int B = st->B, L = st->prompt_len + st->gen_len, blk = sc->block_len;
   if (cora_status e = run_layers(m, st->tokens, B, L, s)) return e;
+  if (gt->persist_scope == 1) {
+    // GLOBAL: score the whole generation region, in chunks of the row workspace, into
+    // top1/conf [B, gen_len]; then the rules read every unresolved position's score
+    const int G = st->gen_len;
+    VocabGateArgs a = vg_args(m->logits, G, st->prompt_len, m->cfg.vocab, m->cfg.mask_id, st,
+                              -1, sc, gt);
+    for (int r0 = 0; r0 < G; r0 += m->max_rows) {
+      const int n = G - r0 < m->max_rows ? G - r0 : m->max_rows;
+      const RowSel sel{1, L, n, st->prompt_len + r0, 0, 0, 0, nullptr};
+      if (cora_status e = lm_head(m, sel, B * n, m->logits, s)) return e;
+      VocabGateArgs c = a;
+      c.n_rows = n;
+      c.out_off = r0;
+      HIP_TRY(launch_vocab_top1(c, s));
+    }
+    HIP_TRY(launch_gate_rules(a, s));
+    return CORA_OK;
+  }
   const RowSel sel{2, L, blk, 0, st->prompt_len, blk, st->gen_len / blk, st->block_idx};
   if (cora_status e = lm_head(m, sel, B * blk, m->logits, s)) return e;
   const VocabGateArgs a = vg_args(m->logits, blk, -1, m->cfg.vocab, m->cfg.mask_id, st, -1, sc,
                                   gt);
-  HIP_TRY(launch_vocab_gate(a, s));
+  HIP_TRY(launch_vocab_top1(a, s));
+  HIP_TRY(launch_gate_rules(a, s));
   return CORA_OK;
 }
 

@@ -192,8 +192,9 @@ __global__ __launch_bounds__(256) void k_vocab_top1(VocabGateArgs a) {
   if (tid == 0) {
     TopState r{sm_m[0], sm_s[0], sm_a[0]};
     for (int w = 1; w < 4; ++w) r = merge(r, TopState{sm_m[w], sm_s[w], sm_a[w]});
-    a.top1[row] = r.arg;
-    a.conf[row] = 1.0f / r.s;
+    const int64_t o = (int64_t)b * a.out_ld + a.out_off + (row - b * a.n_rows);
+    a.top1[o] = r.arg;
+    a.conf[o] = 1.0f / r.s;
   }
 }
 
@@ -215,6 +216,21 @@ __global__ __launch_bounds__(256) void k_gate_rules(VocabGateArgs a) {
   const int row0 = a.row_begin >= 0 ? a.row_begin : lo;
   const bool act = tid < BL;
   const int64_t gi = (int64_t)b * a.L + lo + tid;
+  const bool global = a.persist_scope == 1;
+  if (global) {
+    // Eq. (2) on the scored unresolved positions outside the active block (those inside
+    // are updated below); counters run across blocks
+    for (int j = tid; j < a.n_rows; j += blockDim.x) {
+      const int p = row0 + j;
+      if (p >= lo && p < lo + BL) continue;
+      const int64_t g = (int64_t)b * a.L + p;
+      if (!a.unresolved[g]) continue;
+      const int x = a.top1[(int64_t)b * a.out_ld + j];
+      const int pv = a.prev_top1[g];
+      a.persist[g] = (pv != -1 && pv == x) ? a.persist[g] + 1 : 0;
+      a.prev_top1[g] = x;
+    }
+  }
 
   __shared__ float sc[CORA_MAX_BLOCK];
   __shared__ int su[CORA_MAX_BLOCK];
@@ -222,16 +238,17 @@ __global__ __launch_bounds__(256) void k_gate_rules(VocabGateArgs a) {
   float c = 0.f;
   if (act) {
     U = a.unresolved[gi];
-    const int64_t ri = (int64_t)b * a.n_rows + (lo + tid - row0);
+    const int64_t ri = (int64_t)b * a.out_ld + (lo + tid - row0);
     xh = a.top1[ri];
     c = a.conf[ri];
-    int prev = s == 0 ? -1 : a.prev_top1[gi];
-    int mm = s == 0 ? 0 : a.persist[gi];
+    const bool reset = s == 0 && !global;                 // BLOCK scope: block becomes active
+    int prev = reset ? -1 : a.prev_top1[gi];
+    int mm = reset ? 0 : a.persist[gi];
     if (U) {                                              // Eq. (2)
       mm = (prev != -1 && prev == xh) ? mm + 1 : 0;
       prev = xh;
     }
-    if (s == 0 || U) { a.prev_top1[gi] = prev; a.persist[gi] = mm; }
+    if (reset || U) { a.prev_top1[gi] = prev; a.persist[gi] = mm; }
     m = mm;
     sc[tid] = c;
     su[tid] = U;
@@ -265,16 +282,19 @@ __global__ __launch_bounds__(256) void k_gate_rules(VocabGateArgs a) {
   }
 }
 
-hipError_t launch_vocab_gate(const VocabGateArgs& a, hipStream_t s) {
+hipError_t launch_vocab_top1(const VocabGateArgs& a, hipStream_t s) {
   const int rows = a.B * a.n_rows;
   if (rows == 0) return hipSuccess;
-  if (a.block_len > 256) return hipErrorInvalidValue;  // k_gate_rules: one thread per position
   if (a.V % 8 == 0)
     hipLaunchKernelGGL(k_vocab_top1<true>, dim3(rows), dim3(256), 0, s, a);
   else
     hipLaunchKernelGGL(k_vocab_top1<false>, dim3(rows), dim3(256), 0, s, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  return hipGetLastError();
+}
+
+hipError_t launch_gate_rules(const VocabGateArgs& a, hipStream_t s) {
+  if (a.B == 0) return hipSuccess;
+  if (a.block_len > 256) return hipErrorInvalidValue;  // one thread per block position
   hipLaunchKernelGGL(k_gate_rules, dim3(a.B), dim3(256), 0, s, a);
   return hipGetLastError();
 }

@@ -86,6 +86,6 @@ def test_vocab_gate_rejects_bad_arguments():
     bad_sched = L.SchedCfg(512, 16)
     assert lib.cora_vocab_gate(None, 32, -1, 100, 5, ctypes.byref(st), -1,
                                ctypes.byref(bad_sched), ctypes.byref(gt), None) == -2
-    bad_gate = L.GateCfg(0.65, 1, 1, 1)
+    bad_gate = L.GateCfg(0.65, 1, 1, 2)   # persist_scope: 0 BLOCK, 1 GLOBAL, else unsupported
     assert lib.cora_vocab_gate(None, 32, -1, 100, 5, ctypes.byref(st), -1, ctypes.byref(sc),
                                ctypes.byref(bad_gate), None) == -2

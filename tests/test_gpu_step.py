@@ -194,3 +194,89 @@ def test_free_running_decode(delta_p, m_req, gate_on, blk, steps, spec, min_frac
     assert (final["tokens"][:, P:] != spec.mask_id).all()
     print(f"[summary] steps run {agreed_steps}, first divergence per row {diverged}, "
           f"passes {passes.tolist()}")
+
+
+@pytest.mark.parametrize("spec,min_frac", MODELS)
+@pytest.mark.parametrize("delta_p,m_req,gate_on", [(0.65, 1, True), (0.3, 0, True),
+                                                   (0.0, 1, True), (0.1, 2, True)])
+def test_global_scope_teacher_forced_steps(delta_p, m_req, gate_on, spec, min_frac):
+    """GLOBAL persistence scope (R5): the step scores the whole generation region (LM head
+    and row reduction in chunks), moves every scored unresolved counter, and gates the
+    active block.  Teacher-forced from the oracle's global-scope trajectory."""
+    require_gpu()
+    from paper_2608_11235_amd import DecodeState, Gate, Model, Sched
+    prompt = si.prompt_tokens(1, 1, P, spec.vocab, spec.mask_id)
+    _, _, trace = decode.block_decode(_logits_fn(spec), prompt, G, spec.mask_id, BLK, S, delta_p,
+                                      m_req, gate_on, record=True, scope="global")
+    n_dec = n_dec_ok = 0
+    gen = slice(P, L)
+    with Model(spec, seed=0, max_batch=1, max_seq=L) as m:
+        for si_, step in enumerate(trace):
+            log_case(f"global teacher-forced {spec.name} step {si_} dp={delta_p} m={m_req}")
+            pre, o = step["pre"], step["out"][0]
+            lo = P + o["block"] * BLK
+            ref = step["logits"][0]                                   # rows P .. L-1
+            lg = bf16_to_f32(m.forward_logits(to_dev(pre["tokens"].astype(np.int32)), P, G)
+                             .cpu().numpy())[0].astype(np.float64)
+            Dall = np.max(np.abs(lg - ref), axis=-1)
+            assert Dall.max() <= logit_tolerance(ref), f"step {si_}: logit error {Dall.max()}"
+            st = DecodeState.from_host(pre, P, G, G, BLK)
+            m.denoise_step(st, Sched(BLK, S), Gate(delta_p, m_req, gate_on, 1))
+            gpu = st.to_host()
+            p1_all = margins(ref, spec.mask_id) > 2 * Dall                  # P1, every row
+            assert (gpu["top1"][0][p1_all] == o["x_hat"][p1_all]).all(), f"step {si_} top-1"
+            dlnc = np.abs(np.log(gpu["conf"][0].astype(np.float64)) - np.log(o["c"]))
+            assert (dlnc <= 2 * Dall + CONF_RTOL).all(), f"step {si_} confidence"
+            ob = dict(o, gamma=margins(ref[lo - P:lo - P + BLK], spec.mask_id),
+                      c=o["c"][lo - P:lo - P + BLK])
+            dec_ok, p1 = _comparable(ob, pre["unresolved"][0], lo, Dall[lo - P:lo - P + BLK],
+                                     delta_p, gate_on)
+            # the counter of a block position also needs its whole history certain: teacher
+            # forcing gives both sides the same history, so P1 of this step suffices
+            want = np.zeros(BLK, np.int64)
+            want[np.asarray(o["T"], np.int64) - lo] = 1
+            want[np.asarray(o["A"], np.int64) - lo] = 2
+            assert (gpu["decision"][0][dec_ok] == want[dec_ok]).all(), f"step {si_} decisions"
+            U = pre["unresolved"][0][lo:lo + BLK] == 1
+            n_dec += int(U.sum())
+            n_dec_ok += int((dec_ok & U).sum())
+            nxt = trace[si_ + 1]["pre"] if si_ + 1 < len(trace) else None
+            if nxt is None:
+                continue
+            # counters and previous top-1 of every generation position with a certain top-1
+            for n in ("prev_top1", "persist"):
+                assert (gpu[n][0][gen][p1_all] == nxt[n][0][gen][p1_all]).all(), \
+                    f"step {si_} {n}"
+            outside = np.ones(L, bool)
+            outside[lo:lo + BLK] = False
+            for n in ("tokens", "unresolved"):
+                assert (gpu[n][0][outside] == pre[n][0][outside]).all(), f"step {si_} {n}"
+    print(f"[summary] global scope, steps {len(trace)}: decisions compared {n_dec_ok}/{n_dec}")
+    assert n_dec_ok >= min_frac * n_dec
+
+
+@pytest.mark.parametrize("delta_p,m_req,gate_on", [(0.65, 1, False), (0.0, 0, True),
+                                                   (0.3, 1, True)])
+def test_global_scope_block_decode(delta_p, m_req, gate_on):
+    """block_decode under the GLOBAL scope equals the GPU's own step-by-step trajectory;
+    gate off is the dense decoder, accept-all ends every block in one pass."""
+    require_gpu()
+    from paper_2608_11235_amd import DecodeState, Gate, Model, Sched
+    spec = SEPARATED
+    prompt = si.prompt_tokens(1, 2, P, spec.vocab, spec.mask_id)
+    host = si.initial_decode_state(prompt, G, spec.mask_id)
+    sched, gate = Sched(BLK, S), Gate(delta_p, m_req, gate_on, 1)
+    with Model(spec, seed=0, max_batch=2, max_seq=L) as m:
+        st = DecodeState.from_host(host, P, G, G, BLK)
+        for _ in range((G // BLK) * S):
+            if (st.to_host()["block_idx"] >= G // BLK).all():
+                break
+            m.denoise_step(st, sched, gate)
+        final = st.to_host()
+        out, passes, total = m.block_decode(to_dev(prompt), G, sched, gate)
+    assert (out.cpu().numpy() == final["tokens"]).all() and (passes == final["passes"]).all()
+    assert (final["tokens"][:, P:] != spec.mask_id).all()
+    if not gate_on:
+        assert (passes == S).all()
+    if delta_p <= 0 and m_req == 0:
+        assert (passes == 1).all()

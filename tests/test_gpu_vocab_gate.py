@@ -16,7 +16,7 @@ from tests.parity import CONF_RTOL, bf16_to_f32, comparable_gate, comparable_tra
 pytestmark = pytest.mark.gpu
 
 
-def _oracle(w, k, delta_p, m_req, gate_on, row_begin):
+def _oracle(w, k, delta_p, m_req, gate_on, row_begin, scope="block"):
     """k < 0 -> schedule; row_begin < 0 -> rows follow the active block."""
     st = {n: np.array(v, dtype=np.int64) for n, v in w.state.items()}
     B = w.logits_bits.shape[0]
@@ -27,18 +27,19 @@ def _oracle(w, k, delta_p, m_req, gate_on, row_begin):
         outs.append(decode.step_row(st, b, x, w.prompt_len, w.block_len, w.steps_per_block,
                                     n_blocks, w.mask_id, delta_p, m_req, gate_on,
                                     k_override=None if k < 0 else k,
-                                    logits_row0=None if row_begin < 0 else row_begin))
+                                    logits_row0=None if row_begin < 0 else row_begin,
+                                    scope=scope))
     return st, outs
 
 
-def _gpu(w, k, delta_p, m_req, gate_on, row_begin):
+def _gpu(w, k, delta_p, m_req, gate_on, row_begin, scope="block"):
     from paper_2608_11235_amd import DecodeState, Gate, Sched, vocab_gate
     B, R, V = w.logits_bits.shape
     L = w.state["tokens"].shape[1]
     st = DecodeState.from_host(w.state, w.prompt_len, L - w.prompt_len, R, w.block_len)
     logits = to_dev(w.logits_bits.view(np.int16))
     vocab_gate(logits, R, row_begin, V, w.mask_id, st, k, Sched(w.block_len, w.steps_per_block),
-               Gate(delta_p, m_req, gate_on))
+               Gate(delta_p, m_req, gate_on, 1 if scope == "global" else 0))
     torch.cuda.synchronize()
     return st.to_host()
 
@@ -81,9 +82,9 @@ def _compare(w, gpu, st_or, outs, k, delta_p, gate_on, row_begin):
     return excluded
 
 
-def _check(w, k, delta_p, m_req, gate_on, row_begin=0):
-    gpu = _gpu(w, k, delta_p, m_req, gate_on, row_begin)
-    st_or, outs = _oracle(w, k, delta_p, m_req, gate_on, row_begin)
+def _check(w, k, delta_p, m_req, gate_on, row_begin=0, scope="block"):
+    gpu = _gpu(w, k, delta_p, m_req, gate_on, row_begin, scope)
+    st_or, outs = _oracle(w, k, delta_p, m_req, gate_on, row_begin, scope)
     return _compare(w, gpu, st_or, outs, k, delta_p, gate_on, row_begin), gpu
 
 
@@ -99,6 +100,32 @@ def test_vocab_gate_small(delta_p, m_req, gate_on):
                                masked_in_block=8, spike_max=12.0)
     ex, _ = _check(w, 1, delta_p, m_req, gate_on)
     assert ex <= 1
+
+
+@pytest.mark.parametrize("step0", [False, True])
+@pytest.mark.parametrize("delta_p,m_req,gate_on", [(0.65, 1, True), (0.2, 0, True), (0.0, 1, True),
+                                                   (0.5, 2, True)])
+def test_vocab_gate_global_scope(delta_p, m_req, gate_on, step0):
+    """GLOBAL persistence scope (R5): counters of every scored unresolved position move,
+    inside and outside the active block, and block step 0 does not reset them.  Includes
+    the persistence-only variant (delta_p = 0, m = 1)."""
+    require_gpu()
+    log_case(f"vocab_gate global dp={delta_p} m={m_req} step0={step0}")
+    w = si.vocab_gate_workload(seed=4, batch=5, prompt_len=32, gen_len=128, vocab=3001,
+                               mask_id=17, block_len=32, steps_per_block=8,
+                               masked_in_block=12, spike_max=11.0)
+    if step0:
+        w.state["step_idx"][:] = 0
+    ex, gpu = _check(w, -1, delta_p, m_req, gate_on, 0, "global")
+    assert ex <= 1
+    # positions of later blocks were updated (BLOCK would leave them untouched)
+    moved = 0
+    for b in range(5):
+        hi = 32 + 32 * (int(w.state["block_idx"][b]) + 1)
+        later = np.arange(hi, w.state["tokens"].shape[1])
+        later = later[w.state["unresolved"][b, later] == 1]
+        moved += int((gpu["prev_top1"][b, later] != w.state["prev_top1"][b, later]).sum())
+    assert moved > 0
 
 
 @pytest.mark.parametrize("V", [13, 2047, 2048])
