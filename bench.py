@@ -134,6 +134,93 @@ def vocab_gate_roofline(iters=20):
             "workload": "bf16 logits [8, 512, 126464], k = 1"}
 
 
+def fidelity_run(m, prompt, gen_len, block_len, steps, delta_p, m_req, scope):
+    """Dense decode (gate off) and CORA decode (gate on, persistence scope `scope`) of the
+    same prompts on model m, each timed by wall clock around cora_block_decode; then a
+    step-by-step replay of the (deterministic) CORA decode that records every gate
+    acceptance.  Returns executed passes, rho = CORA / dense passes, speedup, and the
+    fidelity metrics against the dense endpoint: L^out, the fraction of generated
+    positions whose final token differs (Eq. 12), and L^acc, the fraction of gate-accepted
+    tokens that differ from the endpoint at their position (Eq. 7)."""
+    import numpy as np
+    import torch
+
+    import seeded_inputs as si
+    from paper_2608_11235_amd import DecodeState, Gate, Sched
+
+    Bp, Pp = prompt.shape
+    sched = Sched(block_len, steps)
+    pr = torch.from_numpy(prompt).cuda()
+
+    def timed(gate):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        y, passes, total = m.block_decode(pr, gen_len, sched, gate)
+        dt = time.perf_counter() - t0
+        return y.cpu().numpy(), passes, total, dt
+
+    y_d, p_d, tot_d, dt_d = timed(Gate(delta_p, m_req, False))
+    gate = Gate(delta_p, m_req, True, scope)
+    y, p, tot, dt = timed(gate)
+    # replay, recording acceptances (decision 2) at the active block's positions
+    st = DecodeState.from_host(si.initial_decode_state(prompt, gen_len, m.spec.mask_id), Pp,
+                               gen_len, block_len if scope == 0 else gen_len, block_len)
+    n_blocks = gen_len // block_len
+    acc = [[] for _ in range(Bp)]
+    while True:
+        blk = st.block_idx.cpu().numpy().copy()
+        if (blk >= n_blocks).all():
+            break
+        m.denoise_step(st, sched, gate)
+        dec, tok = st.decision.cpu().numpy(), st.tokens.cpu().numpy()
+        for b in range(Bp):
+            if blk[b] < n_blocks:
+                for j in np.nonzero(dec[b] == 2)[0]:
+                    pos = Pp + int(blk[b]) * block_len + int(j)
+                    acc[b].append((pos, int(tok[b, pos])))
+    n_acc = sum(len(a) for a in acc)
+    bad = sum(int(t != y_d[b, i]) for b in range(Bp) for i, t in acc[b])
+    rho = float(p.sum()) / float(p_d.sum())
+    return {
+        "dense": {"passes": int(p_d.sum()), "wall_s": round(dt_d, 3),
+                  "passes_per_s": round(tot_d / dt_d, 2)},
+        "cora": {"passes": int(p.sum()), "passes_per_block": p.tolist(), "rho": round(rho, 4),
+                 "inv_rho": round(1.0 / rho, 3), "wall_s": round(dt, 3),
+                 "speedup_vs_dense": round(dt_d / dt, 3),
+                 "L_out": float(np.mean(y[:, Pp:] != y_d[:, Pp:])), "accepted": n_acc,
+                 "L_acc": bad / n_acc if n_acc else 0.0,
+                 "replay_matches_block_decode": bool((st.tokens.cpu().numpy() == y).all())},
+        "arrays": {"dense_tokens": y_d, "cora_tokens": y, "dense_passes": p_d, "cora_passes": p,
+                   "accepted": acc},
+    }
+
+
+def gated_decode_leg(logit_scale=8.0):
+    """Labelled gate-exercising run (not a paper configuration): the LLaDA-8B shape with
+    random-init logits scaled x8, so top-1 confidences spread and the gate fires.  Dense vs
+    CORA with the BLOCK and the GLOBAL persistence scope (fidelity_run).  With random
+    weights a prediction depends on the whole committed context, so after the first
+    acceptance the CORA trajectory leaves the dense one: L^out / L^acc measure that, not the
+    fidelity a trained model would show."""
+    from dataclasses import replace
+
+    import seeded_inputs as si
+    from paper_2608_11235_amd import LLADA_8B, Model
+
+    spec = replace(LLADA_8B, logit_scale=logit_scale, name=f"llada8b-logits-x{logit_scale:g}")
+    prompt = si.prompt_tokens(1, B, P, spec.vocab, spec.mask_id)
+    out = {"label": f"LLaDA-8B shape, logits x{logit_scale:g} so the gate fires on random "
+                    "weights; not a paper configuration", "gate": [DELTA_P, M_REQ]}
+    with Model(spec, seed=0, max_batch=B, max_seq=P + G) as m:
+        for name, scope in (("cora_block", 0), ("cora_global", 1)):
+            r = fidelity_run(m, prompt, G, BLK, S, DELTA_P, M_REQ, scope)
+            out["dense"] = r["dense"]
+            c = r["cora"]
+            c["L_out"], c["L_acc"] = round(c["L_out"], 4), round(c["L_acc"], 4)
+            out[name] = c
+    return out
+
+
 def copy_calibration(nbytes=1 << 30, iters=5):
     """A plain device-to-device copy of known size: reference for HBM byte counters."""
     import torch
@@ -161,7 +248,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-vocab", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
-    ap.add_argument("--only", choices=["all", "pass", "vocab", "copy"], default="all",
+    ap.add_argument("--no-gated", action="store_true",
+                    help="skip the labelled logits-x8 gated-decode leg")
+    ap.add_argument("--only", choices=["all", "pass", "vocab", "copy", "gated"], default="all",
                     help="run one leg only (profiling runs): the timed passes, the vocab/gate "
                          "kernel, or a plain 1 GiB device copy that calibrates byte counters")
     args = ap.parse_args()
@@ -171,8 +260,11 @@ def main():
     if args.only == "vocab":
         print(json.dumps({"vocab_gate_roofline": vocab_gate_roofline()}), flush=True)
         return
+    if args.only == "gated":
+        print(json.dumps({"gated_decode_logits_x8": gated_decode_leg()}), flush=True)
+        return
     if args.only == "pass":
-        args.no_decode = args.no_vocab = args.no_cpu_baseline = True
+        args.no_decode = args.no_vocab = args.no_cpu_baseline = args.no_gated = True
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (batch rows "
               "decode independently, so more GPUs shard rows with no collective)", file=sys.stderr)
@@ -263,6 +355,8 @@ def main():
 
     if not args.no_vocab:
         result["vocab_gate_roofline"] = vocab_gate_roofline()
+    if not args.no_gated:
+        result["gated_decode_logits_x8"] = gated_decode_leg()
     if not args.no_cpu_baseline:
         import seeded_inputs as si_
         try:
