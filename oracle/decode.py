@@ -29,6 +29,11 @@ Readings of points the paper leaves open (the R-numbers of the design doc):
         ranking are taken on c rounded to fp32, against fp32(delta_p).
     R9  argmax ties -> lowest token id.  R10  the mask id is never predicted.
     R13 gate disabled -> A is empty (the original decoder).
+    R27 EOS-aware controller (EoTP, Table 2): after a step's commits, the lowest
+        committed EOS of the generation region cuts the canvas.  Unresolved positions
+        after it are resolved as EOS (the suffix is removed; committed tokens keep their
+        value).  The active block still decodes its positions before the EOS, then the row
+        stops: no later block is executed.
 """
 import numpy as np
 
@@ -88,7 +93,8 @@ def gate_accept(c32, m, delta_p, m_req):
 
 # --- one denoising step on one batch row ---------------------------------------------------
 def step_row(st, b, logits_blk, prompt_len, block_len, steps_per_block, n_blocks, mask_id,
-             delta_p, m_req, gate_enabled, k_override=None, logits_row0=None, scope="block"):
+             delta_p, m_req, gate_enabled, k_override=None, logits_row0=None, scope="block",
+             eos_id=None):
     """Apply the decision part of one executed step to batch row b, in place.
 
     logits_blk [n_rows, V] are the logits of canvas rows starting at `logits_row0`
@@ -140,14 +146,26 @@ def step_row(st, b, logits_blk, prompt_len, block_len, steps_per_block, n_blocks
     fixed = np.union1d(T, A)                                               # Eq. (4)
     st["tokens"][b, fixed] = x_hat[fixed]
     st["unresolved"][b, fixed] = 0
+    removed, cut = np.zeros(0, dtype=np.int64), None
+    if eos_id is not None:                                                 # R27
+        L = st["tokens"].shape[1]
+        gen = np.arange(prompt_len, L)
+        eos = gen[(st["unresolved"][b, gen] == 0) & (st["tokens"][b, gen] == eos_id)]
+        if len(eos):
+            cut = int(eos.min())
+            later = np.arange(cut + 1, L)
+            removed = later[st["unresolved"][b, later] == 1]
+            st["tokens"][b, removed] = eos_id
+            st["unresolved"][b, removed] = 0
     done = not st["unresolved"][b, pos].any()                              # termination
     st["step_idx"][b] = s + 1
     if done:
-        st["block_idx"][b] = blk + 1
+        st["block_idx"][b] = n_blocks if cut is not None else blk + 1
         st["step_idx"][b] = 0
     return {"finished": False, "x_hat": x_hat_rows, "c": c_rows, "c32": c_rows.astype(np.float32),
             "T": T, "A": A, "done": done, "block": blk, "step": s, "k": int(k),
-            "residual": residual, "m": st["persist"][b].copy()}
+            "residual": residual, "m": st["persist"][b].copy(),
+            "removed": removed, "eos_cut": cut}
 
 
 def block_positions(st, b, prompt_len, block_len, n_blocks):
@@ -162,14 +180,14 @@ def copy_state(st):
 
 # --- the gated block decode (Fig. 2; Section 3, "From acceptance to runtime") -----------
 def block_decode(logits_fn, prompt, gen_len, mask_id, block_len, steps_per_block,
-                 delta_p, m_req, gate_enabled, record=False, scope="block"):
+                 delta_p, m_req, gate_enabled, record=False, scope="block", eos_id=None):
     """Decode every batch row independently (R15), block by block, left to right.
 
     logits_fn(tokens [B, L], rows list-of-arrays) -> list of [len(rows_b), V] logits.
     Each executed step runs one dense pass, then the decision rules; a block ends
     once it holds no unresolved position, skipping its remaining passes.  The block
     scope scores the active block's rows, the global scope the whole generation
-    region (R5).
+    region (R5).  eos_id enables the EOS-aware controller (R27).
 
     Returns (tokens [B, L], passes [B, n_blocks], trace) where trace holds the
     pre-step state and step outputs of every executed pass when record=True."""
@@ -202,15 +220,17 @@ def block_decode(logits_fn, prompt, gen_len, mask_id, block_len, steps_per_block
             blk = int(st["block_idx"][b])
             outs[b] = step_row(st, b, logits[b], P, block_len, steps_per_block, n_blocks,
                                mask_id, delta_p, m_req, gate_enabled,
-                               logits_row0=int(rows[b][0]), scope=scope)
+                               logits_row0=int(rows[b][0]), scope=scope, eos_id=eos_id)
             passes[b, blk] += 1
         if record:
             trace.append({"pre": pre, "rows": rows, "logits": logits, "out": outs})
     return st["tokens"], passes, trace
 
 
-def dense_endpoint(logits_fn, prompt, gen_len, mask_id, block_len, steps_per_block):
-    """Y*: the original fixed-horizon decoder = the block decode with the gate disabled."""
+def dense_endpoint(logits_fn, prompt, gen_len, mask_id, block_len, steps_per_block,
+                   eos_id=None):
+    """Y*: the original fixed-horizon decoder = the block decode with the gate disabled
+    (with eos_id: the EOS-aware dense decoder, R27)."""
     tokens, passes, _ = block_decode(logits_fn, prompt, gen_len, mask_id, block_len,
-                                     steps_per_block, 1.0, 0, gate_enabled=False)
+                                     steps_per_block, 1.0, 0, gate_enabled=False, eos_id=eos_id)
     return tokens, passes

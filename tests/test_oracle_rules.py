@@ -249,3 +249,83 @@ def test_global_scope_worked_example():
     assert [o["out"][0]["T"].tolist() for o in tr_g] == [[1], [2], [3]]
     assert [o["out"][0]["A"].tolist() for o in tr_g] == [[], [], [4]]
     assert tr_g[2]["out"][0]["m"][4] == 2 and tr_b[3]["out"][0]["m"][4] == 1
+
+
+def _eotp_script_fn(logit_of_pos, V):
+    """Every pass: position p's logits are fixed (token, logit) pairs, other entries 0."""
+    def fn(tokens, rows):
+        out = []
+        for r in rows:
+            l = np.zeros((len(r), V))
+            for j, p in enumerate(r):
+                for tok, val in logit_of_pos.get(int(p), []):
+                    l[j, tok] = val
+            out.append(l)
+        return out
+    return fn
+
+
+def test_eotp_worked_example():
+    """Hand-worked (R27): V = 4 (tokens 0, 1; EOS 2; mask 3), prompt 1, gen 6, blocks of 2,
+    S = 2 (k_s = 1, 1).  Position 1 -> token 0 (logit 3, c = e^3/(e^3+2) = 0.909),
+    position 2 -> EOS (logit 5, c = 0.987), position 3 -> token 1 (logit 4), 4-6 -> token 0
+    (logit 2).
+      fixed horizon, gate off: every block takes 2 passes; output 0 EOS 1 0 0 0.
+      EoTP, gate off: pass 1 transfers the EOS at 2 (highest c) -> positions 3-6 become EOS;
+        pass 2 transfers position 1 -> block done, row stops: passes (2, 0, 0).
+      EoTP, gate (0.6, m = 0): pass 1 transfers the EOS and accepts position 1 -> (1, 0, 0)."""
+    V, EOS, MASK = 4, 2, 3
+    script = {1: [(0, 3.0)], 2: [(EOS, 5.0)], 3: [(1, 4.0)], 4: [(0, 2.0)], 5: [(0, 2.0)],
+              6: [(0, 2.0)]}
+    fn = _eotp_script_fn(script, V)
+    prompt = np.array([[1]])
+    t, p, _ = decode.block_decode(fn, prompt, 6, MASK, 2, 2, 0.6, 0, False)
+    assert p.tolist() == [[2, 2, 2]] and t.tolist() == [[1, 0, EOS, 1, 0, 0, 0]]
+    t, p, tr = decode.block_decode(fn, prompt, 6, MASK, 2, 2, 0.6, 0, False, record=True,
+                                   eos_id=EOS)
+    assert p.tolist() == [[2, 0, 0]] and t.tolist() == [[1, 0, EOS, EOS, EOS, EOS, EOS]]
+    assert tr[0]["out"][0]["eos_cut"] == 2 and tr[0]["out"][0]["removed"].tolist() == [3, 4, 5, 6]
+    t, p, _ = decode.block_decode(fn, prompt, 6, MASK, 2, 2, 0.6, 0, True, eos_id=EOS)
+    assert p.tolist() == [[1, 0, 0]] and t.tolist() == [[1, 0, EOS, EOS, EOS, EOS, EOS]]
+
+
+@pytest.mark.parametrize("gate", [False, True])
+@pytest.mark.parametrize("seed", range(5))
+def test_eotp_follows_fixed_horizon_until_eos(seed, gate):
+    """Until the step that commits the first EOS, the EOS-aware decode is the fixed-horizon
+    one; afterwards no later block runs and every later position is EOS unless it was
+    committed before the cut.  The EOS id is taken from the fixed-horizon output so it
+    occurs."""
+    V, P, G, blk, S = 17, 3, 32, 8, 4
+    model = _RandomModel(V, P + G, seed, scale=2.0)
+    prompt = np.random.default_rng(seed).integers(0, V - 1, (1, P))
+    t_fh, p_fh, tr_fh = decode.block_decode(model, prompt, G, V - 1, blk, S, 0.5, 1, gate,
+                                            record=True)
+    eos = int(t_fh[0, P + G // 2])
+    t_e, p_e, tr_e = decode.block_decode(model, prompt, G, V - 1, blk, S, 0.5, 1, gate,
+                                         record=True, eos_id=eos)
+    first = next(i for i, s in enumerate(tr_e) if s["out"][0]["eos_cut"] is not None)
+    for a, b in zip(tr_fh[:first + 1], tr_e[:first + 1]):   # same states and decisions
+        assert (a["pre"]["tokens"] == b["pre"]["tokens"]).all()
+        assert a["out"][0]["T"].tolist() == b["out"][0]["T"].tolist()
+        assert a["out"][0]["A"].tolist() == b["out"][0]["A"].tolist()
+    cut = tr_e[-1]["out"][0]["eos_cut"]
+    assert t_e[0, cut] == eos and not (t_e[0, P:cut] == eos).any()
+    cut_blk = (cut - P) // blk
+    assert (p_e[0, cut_blk + 1:] == 0).all() and (p_e[0, :cut_blk] == p_fh[0, :cut_blk]).all()
+    pre_cut = tr_e[first]["pre"]
+    committed = pre_cut["unresolved"][0] == 0
+    for i in range(cut + 1, P + G):
+        assert t_e[0, i] == eos or committed[i] or i in np.union1d(
+            tr_e[first]["out"][0]["T"], tr_e[first]["out"][0]["A"])
+    assert p_e.sum() <= p_fh.sum()
+
+
+def test_eotp_unpredictable_eos_is_fixed_horizon():
+    """An EOS id that is never predicted (the mask id) leaves the decoder unchanged."""
+    V, P, G, blk, S = 13, 2, 16, 8, 4
+    model = _RandomModel(V, P + G, 1, scale=2.0)
+    prompt = np.random.default_rng(1).integers(0, V - 1, (2, P))
+    a = decode.block_decode(model, prompt, G, V - 1, blk, S, 0.4, 1, True)
+    b = decode.block_decode(model, prompt, G, V - 1, blk, S, 0.4, 1, True, eos_id=V - 1)
+    assert (a[0] == b[0]).all() and (a[1] == b[1]).all()
