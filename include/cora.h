@@ -66,9 +66,17 @@ typedef struct {
  * steps_per_block executed steps (Section 3, "Diffusion Decoding Setup").
  * The transfer rule fixes k_s = floor(block_len / S) + [s < block_len mod S]
  * positions at block step s (a linear split of the block's masked positions).
- * 1 <= steps_per_block <= block_len <= CORA_MAX_BLOCK_LEN. */
+ * 1 <= steps_per_block <= block_len <= CORA_MAX_BLOCK_LEN.
+ * eos_enabled != 0 turns on the EOS-aware controller of the deployment runs
+ * (Table 2): after a step's commits, the lowest committed eos_id in the
+ * generation region cuts the canvas; unresolved positions after it are
+ * resolved as eos_id (decision code 3 inside the active block), committed
+ * tokens keep their value, the active block finishes its positions before the
+ * EOS and the row then stops (block_idx = number of blocks).  eos_enabled = 0
+ * (a zero-initialised struct) keeps the fixed horizon. */
 typedef struct {
   int32_t block_len, steps_per_block;
+  int32_t eos_enabled, eos_id;
 } cora_sched_cfg;
 
 /* Residual gate of Eq. (3): accept i iff c_i >= delta_p and m_i >= m_req,

@@ -24,7 +24,8 @@ class ModelCfg(ctypes.Structure):
 
 
 class SchedCfg(ctypes.Structure):
-    _fields_ = [("block_len", c_i32), ("steps_per_block", c_i32)]
+    _fields_ = [("block_len", c_i32), ("steps_per_block", c_i32), ("eos_enabled", c_i32),
+                ("eos_id", c_i32)]
 
 
 class GateCfg(ctypes.Structure):

@@ -1,5 +1,6 @@
 """Pythonic wrappers over the C ABI (marshalling only)."""
 import ctypes
+from typing import Optional
 from dataclasses import dataclass
 
 import numpy as np
@@ -30,9 +31,12 @@ def model_cfg_from(spec) -> _lib.ModelCfg:
 class Sched:
     block_len: int = 32
     steps_per_block: int = 32
+    eos_id: Optional[int] = None   # EOS-aware controller when set
 
     def c(self):
-        return _lib.SchedCfg(self.block_len, self.steps_per_block)
+        return _lib.SchedCfg(self.block_len, self.steps_per_block,
+                             0 if self.eos_id is None else 1,
+                             0 if self.eos_id is None else int(self.eos_id))
 
 
 @dataclass

@@ -102,6 +102,7 @@ struct VocabGateArgs {
   float delta_p; int m_req; int gate_enabled;
   int persist_scope;  // 0 BLOCK, 1 GLOBAL (every scored unresolved position, no block reset)
   int out_ld, out_off;
+  int eos_enabled, eos_id;  // EOS-aware controller
 };
 // top-1 and confidence of every logits row
 hipError_t launch_vocab_top1(const VocabGateArgs& a, hipStream_t s);

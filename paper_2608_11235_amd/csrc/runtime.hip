@@ -479,6 +479,8 @@ static VocabGateArgs vg_args(const uint16_t* logits, int n_rows, int row_begin, 
   a.persist_scope = gt->persist_scope;
   a.out_ld = n_rows;
   a.out_off = 0;
+  a.eos_enabled = sc->eos_enabled ? 1 : 0;
+  a.eos_id = sc->eos_id;
   return a;
 }
 
@@ -490,6 +492,8 @@ extern "C" cora_status cora_vocab_gate(const uint16_t* d_logits, int32_t n_rows,
   if (cora_status e = check_state(st, sc)) return e;
   if (!d_logits) return fail(CORA_ERR_INVALID_ARG, "null logits");
   if (V < 2 || mask_id < 0 || mask_id >= V) return fail(CORA_ERR_INVALID_ARG, "bad V/mask_id");
+  if (sc->eos_enabled && (sc->eos_id < 0 || sc->eos_id >= V))
+    return fail(CORA_ERR_INVALID_ARG, "eos_id must lie in [0, V)");
   const int L = st->prompt_len + st->gen_len;
   if (row_begin >= 0) {
     if (row_begin > st->prompt_len || row_begin + n_rows < L || row_begin + n_rows > L)
@@ -548,6 +552,8 @@ static cora_status check_step(cora_model* m, const cora_state* st, const cora_sc
     return fail(CORA_ERR_INVALID_ARG, "state exceeds the model's max_batch / max_seq");
   if (sc->block_len > m->max_rows)
     return fail(CORA_ERR_INVALID_ARG, "block_len exceeds the model's row workspace");
+  if (sc->eos_enabled && (sc->eos_id < 0 || sc->eos_id >= m->cfg.vocab))
+    return fail(CORA_ERR_INVALID_ARG, "eos_id must lie in [0, vocab)");
   return CORA_OK;
 }
 

@@ -15,8 +15,10 @@
 //   Eq. (2) counter update on unresolved positions;
 //   transfer rule: the k highest-confidence unresolved positions (ties -> lower position);
 //   Eq. (3) gate on the other unresolved positions (c >= delta_p and m >= m_req);
-//   Eq. (4) commit of both sets; block done once no unresolved position is left,
-//   then the row moves to its next block.
+//   Eq. (4) commit of both sets; with the EOS-aware controller, the lowest committed EOS
+//   of the generation region cuts the canvas (later unresolved positions resolved as EOS);
+//   block done once no unresolved position is left, then the row moves to its next block
+//   (or stops after an EOS cut).
 // Splitting the two removes a per-row tail (agent-coherent result stores, their
 // completion, a ticket round trip) from every workgroup of the bandwidth-bound first pass.
 #include <limits.h>
@@ -269,11 +271,37 @@ __global__ __launch_bounds__(256) void k_gate_rules(VocabGateArgs a) {
     }
   }
   if (act) a.decision[(int64_t)b * BL + tid] = T ? 1 : (A ? 2 : 0);
-  const int left = __syncthreads_or(act && U && !(T || A));
+  // EOS-aware controller: the lowest committed EOS of the generation region cuts the
+  // canvas; later unresolved positions are resolved as EOS and the row stops after this
+  // block
+  __shared__ int s_cut;
+  int cut = INT_MAX;
+  if (a.eos_enabled) {
+    if (tid == 0) s_cut = INT_MAX;
+    __syncthreads();  // this step's commits are visible to the whole workgroup
+    for (int p = a.prompt_len + tid; p < a.L; p += blockDim.x) {
+      const int64_t g = (int64_t)b * a.L + p;
+      if (!a.unresolved[g] && a.tokens[g] == a.eos_id) atomicMin(&s_cut, p);
+    }
+    __syncthreads();
+    cut = s_cut;
+    if (cut != INT_MAX) {
+      for (int p = cut + 1 + tid; p < a.L; p += blockDim.x) {
+        const int64_t g = (int64_t)b * a.L + p;
+        if (a.unresolved[g]) {
+          a.tokens[g] = a.eos_id;
+          a.unresolved[g] = 0;
+          if (p >= lo && p < lo + BL) a.decision[(int64_t)b * BL + (p - lo)] = 3;
+        }
+      }
+    }
+  }
+  const bool cut_off = cut != INT_MAX && lo + tid > cut;
+  const int left = __syncthreads_or(act && U && !(T || A) && !cut_off);
   if (tid == 0) {
     if (a.passes) a.passes[(int64_t)b * a.n_blocks + blk] += 1;
     if (!left) {
-      a.block_idx[b] = blk + 1;
+      a.block_idx[b] = cut != INT_MAX ? a.n_blocks : blk + 1;
       a.step_idx[b] = 0;
     } else {
       a.step_idx[b] = s + 1;

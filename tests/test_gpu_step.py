@@ -280,3 +280,99 @@ def test_global_scope_block_decode(delta_p, m_req, gate_on):
         assert (passes == S).all()
     if delta_p <= 0 and m_req == 0:
         assert (passes == 1).all()
+
+
+@pytest.mark.parametrize("scope", [0, 1])
+@pytest.mark.parametrize("delta_p,m_req,gate_on", [(0.65, 1, False), (0.3, 1, True)])
+def test_eos_aware_teacher_forced_steps(delta_p, m_req, gate_on, scope):
+    """EOS-aware controller (R27), teacher-forced from the oracle's EOS-aware trajectory on
+    the separated tiny model; the EOS id is a token of the oracle's fixed-horizon output in
+    block 0, so a cut happens.  Decisions are compared where the logit error cannot flip them
+    (P1-P3); the removals of a step (decision 3) and the stop are compared where the cut is
+    certain: every unresolved block position up to it has a certain decision and top-1."""
+    require_gpu()
+    from paper_2608_11235_amd import DecodeState, Gate, Model, Sched
+    spec = SEPARATED
+    sc = "global" if scope else "block"
+    prompt = si.prompt_tokens(1, 1, P, spec.vocab, spec.mask_id)
+    fn = _logits_fn(spec)
+    t_fh, _, _ = decode.block_decode(fn, prompt, G, spec.mask_id, BLK, S, delta_p, m_req,
+                                     gate_on, scope=sc)
+    eos = int(t_fh[0, P + 20])
+    _, passes_or, trace = decode.block_decode(fn, prompt, G, spec.mask_id, BLK, S, delta_p,
+                                              m_req, gate_on, record=True, scope=sc,
+                                              eos_id=eos)
+    assert any(s["out"][0]["eos_cut"] is not None for s in trace)
+    n_dec = n_ok = cuts_checked = 0
+    with Model(spec, seed=0, max_batch=1, max_seq=L) as m:
+        for si_, step in enumerate(trace):
+            log_case(f"eos-aware teacher-forced step {si_} scope={sc} gate={gate_on}")
+            pre, o = step["pre"], step["out"][0]
+            lo = P + o["block"] * BLK
+            r0 = lo if scope == 0 else P
+            n = BLK if scope == 0 else G
+            ref = step["logits"][0]
+            lg = bf16_to_f32(m.forward_logits(to_dev(pre["tokens"].astype(np.int32)), r0, n)
+                             .cpu().numpy())[0].astype(np.float64)
+            D = np.max(np.abs(lg - ref), axis=-1)
+            assert D.max() <= logit_tolerance(ref)
+            st = DecodeState.from_host(pre, P, G, n, BLK)
+            m.denoise_step(st, Sched(BLK, S, eos), Gate(delta_p, m_req, gate_on, scope))
+            gpu = st.to_host()
+            ob = dict(o, gamma=margins(ref[lo - r0:lo - r0 + BLK], spec.mask_id),
+                      c=o["c"][lo - r0:lo - r0 + BLK])
+            dec_ok, p1 = _comparable(ob, pre["unresolved"][0], lo, D[lo - r0:lo - r0 + BLK],
+                                     delta_p, gate_on)
+            U = pre["unresolved"][0][lo:lo + BLK] == 1
+            want = np.zeros(BLK, np.int64)
+            want[np.asarray(o["T"], np.int64) - lo] = 1
+            want[np.asarray(o["A"], np.int64) - lo] = 2
+            rem = np.asarray(o["removed"], np.int64)
+            rem_blk = rem[(rem >= lo) & (rem < lo + BLK)] - lo
+            cut = o["eos_cut"]
+            end = BLK if cut is None or cut >= lo + BLK else max(cut - lo + 1, 0)
+            cut_certain = bool((dec_ok & p1)[:end][U[:end]].all())
+            cmp = dec_ok & U
+            if not cut_certain:
+                cmp[rem_blk] = False
+            want[rem_blk] = 3
+            assert (gpu["decision"][0][cmp] == want[cmp]).all(), f"step {si_} decisions"
+            n_dec += int(U.sum())
+            n_ok += int(cmp.sum())
+            nxt = trace[si_ + 1]["pre"] if si_ + 1 < len(trace) else None
+            if cut is not None and cut_certain and (dec_ok & p1)[U].all() and nxt is not None:
+                for k in ("tokens", "unresolved", "block_idx", "step_idx"):
+                    assert (gpu[k][0] == nxt[k][0]).all(), f"step {si_} {k}"
+                cuts_checked += 1
+    print(f"[summary] eos-aware scope={sc}: decisions compared {n_ok}/{n_dec}, "
+          f"whole-state checks after a cut {cuts_checked}, oracle passes {passes_or.tolist()}")
+    assert n_ok >= 0.3 * n_dec
+
+
+@pytest.mark.parametrize("scope", [0, 1])
+def test_eos_aware_block_decode(scope):
+    """block_decode with the EOS-aware controller equals the GPU's own step-by-step
+    trajectory; no block after the cut runs and nothing after the cut stays masked."""
+    require_gpu()
+    from paper_2608_11235_amd import DecodeState, Gate, Model, Sched
+    spec = SEPARATED
+    prompt = si.prompt_tokens(1, 2, P, spec.vocab, spec.mask_id)
+    host = si.initial_decode_state(prompt, G, spec.mask_id)
+    gate = Gate(0.3, 1, True, scope)
+    with Model(spec, seed=0, max_batch=2, max_seq=L) as m:
+        y0, _, _ = m.block_decode(to_dev(prompt), G, Sched(BLK, S), gate)
+        eos = int(y0.cpu().numpy()[0, P + 10])
+        sched = Sched(BLK, S, eos)
+        st = DecodeState.from_host(host, P, G, BLK if scope == 0 else G, BLK)
+        for _ in range((G // BLK) * S):
+            if (st.to_host()["block_idx"] >= G // BLK).all():
+                break
+            m.denoise_step(st, sched, gate)
+        final = st.to_host()
+        out, passes, total = m.block_decode(to_dev(prompt), G, sched, gate)
+    y = out.cpu().numpy()
+    assert (y == final["tokens"]).all() and (passes == final["passes"]).all()
+    gen = y[0, P:]
+    cut = int(np.nonzero(gen == eos)[0][0])
+    assert (passes[0, cut // BLK + 1:] == 0).all()
+    assert (gen != spec.mask_id).all() and (y[1, P:] != spec.mask_id).all()

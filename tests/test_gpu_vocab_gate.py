@@ -16,7 +16,7 @@ from tests.parity import CONF_RTOL, bf16_to_f32, comparable_gate, comparable_tra
 pytestmark = pytest.mark.gpu
 
 
-def _oracle(w, k, delta_p, m_req, gate_on, row_begin, scope="block"):
+def _oracle(w, k, delta_p, m_req, gate_on, row_begin, scope="block", eos_id=None):
     """k < 0 -> schedule; row_begin < 0 -> rows follow the active block."""
     st = {n: np.array(v, dtype=np.int64) for n, v in w.state.items()}
     B = w.logits_bits.shape[0]
@@ -28,17 +28,18 @@ def _oracle(w, k, delta_p, m_req, gate_on, row_begin, scope="block"):
                                     n_blocks, w.mask_id, delta_p, m_req, gate_on,
                                     k_override=None if k < 0 else k,
                                     logits_row0=None if row_begin < 0 else row_begin,
-                                    scope=scope))
+                                    scope=scope, eos_id=eos_id))
     return st, outs
 
 
-def _gpu(w, k, delta_p, m_req, gate_on, row_begin, scope="block"):
+def _gpu(w, k, delta_p, m_req, gate_on, row_begin, scope="block", eos_id=None):
     from paper_2608_11235_amd import DecodeState, Gate, Sched, vocab_gate
     B, R, V = w.logits_bits.shape
     L = w.state["tokens"].shape[1]
     st = DecodeState.from_host(w.state, w.prompt_len, L - w.prompt_len, R, w.block_len)
     logits = to_dev(w.logits_bits.view(np.int16))
-    vocab_gate(logits, R, row_begin, V, w.mask_id, st, k, Sched(w.block_len, w.steps_per_block),
+    vocab_gate(logits, R, row_begin, V, w.mask_id, st, k,
+               Sched(w.block_len, w.steps_per_block, eos_id),
                Gate(delta_p, m_req, gate_on, 1 if scope == "global" else 0))
     torch.cuda.synchronize()
     return st.to_host()
@@ -72,6 +73,8 @@ def _compare(w, gpu, st_or, outs, k, delta_p, gate_on, row_begin):
         dec = np.zeros(w.block_len, np.int64)
         dec[o["T"] - lo] = 1
         dec[o["A"] - lo] = 2
+        rem = np.asarray(o.get("removed", []), np.int64)
+        dec[rem[(rem >= lo) & (rem < lo + w.block_len)] - lo] = 3
         assert (gpu["decision"][b] == dec).all(), f"batch row {b} decisions"
         for n in ("tokens", "unresolved", "prev_top1", "persist"):
             assert (gpu[n][b] == st_or[n][b]).all(), f"batch row {b} {n}"
@@ -82,9 +85,9 @@ def _compare(w, gpu, st_or, outs, k, delta_p, gate_on, row_begin):
     return excluded
 
 
-def _check(w, k, delta_p, m_req, gate_on, row_begin=0, scope="block"):
-    gpu = _gpu(w, k, delta_p, m_req, gate_on, row_begin, scope)
-    st_or, outs = _oracle(w, k, delta_p, m_req, gate_on, row_begin, scope)
+def _check(w, k, delta_p, m_req, gate_on, row_begin=0, scope="block", eos_id=None):
+    gpu = _gpu(w, k, delta_p, m_req, gate_on, row_begin, scope, eos_id)
+    st_or, outs = _oracle(w, k, delta_p, m_req, gate_on, row_begin, scope, eos_id)
     return _compare(w, gpu, st_or, outs, k, delta_p, gate_on, row_begin), gpu
 
 
@@ -126,6 +129,32 @@ def test_vocab_gate_global_scope(delta_p, m_req, gate_on, step0):
         later = later[w.state["unresolved"][b, later] == 1]
         moved += int((gpu["prev_top1"][b, later] != w.state["prev_top1"][b, later]).sum())
     assert moved > 0
+
+
+@pytest.mark.parametrize("scope", ["block", "global"])
+def test_vocab_gate_eos_aware(scope):
+    """EOS-aware controller (R27): the EOS id is the top-1 of the highest-confidence
+    unresolved position of batch row 0's block, so the transfer rule commits it there; the
+    cut resolves every later unresolved position as EOS (decision 3 inside the block) and
+    the row stops once its block is done.  Every state array must equal the oracle's."""
+    require_gpu()
+    log_case(f"vocab_gate eos-aware scope={scope}")
+    w = si.vocab_gate_workload(seed=8, batch=4, prompt_len=16, gen_len=96, vocab=2000,
+                               mask_id=1999, block_len=32, steps_per_block=4,
+                               masked_in_block=20, spike_max=12.0)
+    st0, outs0 = _oracle(w, 2, 0.5, 1, True, 0, scope)
+    b0 = outs0[0]
+    lo = 16 + 32 * int(w.state["block_idx"][0])
+    T0 = np.asarray(b0["T"], np.int64)
+    c_blk = b0["c"][T0]                       # rows start at canvas position 0
+    eos = int(b0["x_hat"][T0[np.argmax(c_blk)]])
+    ex, gpu = _check(w, 2, 0.5, 1, True, 0, scope, eos)
+    assert ex <= 1
+    st_or, outs = _oracle(w, 2, 0.5, 1, True, 0, scope, eos)
+    cut = outs[0]["eos_cut"]
+    assert cut is not None
+    assert not gpu["unresolved"][0, cut + 1:].any()
+    assert gpu["tokens"][0, cut] == eos
 
 
 @pytest.mark.parametrize("V", [13, 2047, 2048])
