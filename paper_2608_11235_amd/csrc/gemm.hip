@@ -50,6 +50,17 @@ constexpr int LDK = BK + 8;  // padded LDS row, in bf16 elements
 // n 16-byte loads at byte offset voff + i * step (step uniform) through a buffer resource;
 // when the chunks do not divide evenly, the last one exists only for threads with
 // tid + (N-1) * NT < total.
+// n 16-byte loads, the last one from its own per-lane base (an out-of-range base makes the
+// hardware return zeros without touching memory)
+template <int N>
+__device__ __forceinline__ void buf_load_tail(u32x4_t (&r)[N], __amdgpu_buffer_rsrc_t rs, int voff,
+                                              int voff_last, int step) {
+#pragma unroll
+  for (int i = 0; i < N; ++i)
+    r[i] = __builtin_bit_cast(
+        u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, i + 1 < N ? voff : voff_last, i * step, 0));
+}
+
 template <int N, bool EXACT>
 __device__ __forceinline__ void buf_load(u32x4_t (&r)[N], __amdgpu_buffer_rsrc_t rs, int voff,
                                          int step, bool last_ok) {
@@ -182,10 +193,14 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void k_gemm(GemmArgs g) {
     };
     // all chunks of every thread: rows past the tile read real rows or the range-checked
     // zeros past M / N, and are stored to the spare LDS rows
-#define FETCH_ALL(ra, rb, kt)                                          \
-  do {                                                                 \
-    buf_load<CA, true>(ra, a_rs, a_off + (kt) * BK * 2, a_step, true); \
-    buf_load<CB, true>(rb, b_rs, b_off + (kt) * BK * 2, b_step, true); \
+    // a thread's chunk past the tile (CA * NT / 8 > BM) reads from the first byte past the
+    // operand: zeros, no memory traffic
+    const int a_tail = A_EXACT || a_last ? a_off : (int)(a_bytes > 0x7fffffffLL ? 0x7fffffff : a_bytes);
+    const int b_tail = B_EXACT || b_last ? b_off : (int)(b_bytes > 0x7fffffffLL ? 0x7fffffff : b_bytes);
+#define FETCH_ALL(ra, rb, kt)                                                              \
+  do {                                                                                     \
+    buf_load_tail<CA>(ra, a_rs, a_off + (kt) * BK * 2, a_tail + (kt) * BK * 2, a_step);    \
+    buf_load_tail<CB>(rb, b_rs, b_off + (kt) * BK * 2, b_tail + (kt) * BK * 2, b_step);    \
   } while (0)
 #define SG(mask, n) __builtin_amdgcn_sched_group_barrier(mask, n, 0)
     // slice KT out of LDS buffer KT & 1; RAN/RBN hold slice KT+1 on entry and receive
