@@ -138,14 +138,20 @@ typedef struct cora_model cora_model;
  * with mix the SplitMix64 finaliser and G = 0x9E3779B97F4A7C15.  Tensor ids:
  * 1 embedding [V, d], 2 LM head [V, d], and 100 + 16 l + j for layer l with
  * j = 0 wq, 1 wk, 2 wv, 3 wo, 4 wg, 5 wu, 6 wd, 7 bq, 8 bk, 9 bv.  Norm
- * weights are 1.  Synchronous.  *out is set only on success. */
+ * weights are 1.  The LM head is also kept in a second, packed layout (the
+ * order in which the few-row LM-head kernel streams it: 32-row groups of 1 KB
+ * MFMA operand blocks), written once here: weight bytes include one more
+ * V x d bf16 matrix.  Synchronous.  *out is set only on success. */
 cora_status cora_model_create(const cora_model_cfg *cfg, uint64_t seed, int32_t max_batch,
                               int32_t max_seq, void *hip_stream, cora_model **out);
 cora_status cora_model_destroy(cora_model *model);
 
 /* Dense forward pass over tokens [B, L] (int32, device) and the LM head on
  * canvas rows [row_begin, row_begin + n_rows) of every batch row: writes
- * bf16 logits [B, n_rows, V] (device, caller-allocated).  Parity hook. */
+ * bf16 logits [B, n_rows, V] (device, caller-allocated).  Up to 64 rows
+ * (B * n_rows) go through the few-row LM-head kernel, more through the tiled
+ * GEMM; both round (sum_k a_k w_k) * logit_scale to bf16 and differ only in
+ * fp32 summation order.  Parity hook. */
 cora_status cora_forward_logits(cora_model *model, const int32_t *d_tokens, int32_t B, int32_t L,
                                 int32_t row_begin, int32_t n_rows, uint16_t *d_logits,
                                 void *hip_stream);
@@ -155,7 +161,12 @@ cora_status cora_forward_logits(cora_model *model, const int32_t *d_tokens, int3
  * vocab/gate kernels (Eq. 1, Eq. 2, transfer rule, Eq. 3, Eq. 4, termination;
  * see cora_vocab_gate).  top1/conf are [B, block_len] (the active block's
  * rows) under the BLOCK scope and [B, gen_len] (the generation region, LM head
- * and row reduction in chunks of up to 256 rows) under GLOBAL.  Asynchronous. */
+ * and row reduction in chunks of up to 256 rows) under GLOBAL.  When a call
+ * (or chunk) scores at most 64 rows in all, Eq. (1) is computed inside the
+ * LM-head pass (per-128-entry partial max / first arg max / sum of exp,
+ * merged in vocab order) and no logits are written; the top-1 is then the
+ * same as cora_vocab_gate's on the logits cora_forward_logits writes for
+ * those rows.  Asynchronous. */
 cora_status cora_denoise_step(cora_model *model, cora_state *state, const cora_sched_cfg *sched,
                               const cora_gate_cfg *gate, void *hip_stream);
 

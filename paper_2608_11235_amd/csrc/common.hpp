@@ -50,3 +50,29 @@ __device__ __forceinline__ float warp_sum(float v) {
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
   return v;
 }
+
+// ---- softmax statistics of a row (Eq. 1) ---------------------------------------------------
+// Partial (max, sum of exp(l - max), lowest index holding the max) over a set of logits;
+// an empty set is (-inf, 0, INT_MAX).
+struct TopState {
+  float m, s;
+  int arg;
+};
+
+constexpr float LOG2E = 1.4426950408889634f;
+
+// 2^x with the hardware v_exp_f32: results below 2^-126 flush to zero, which cannot change
+// a softmax sum that already holds the max term (1.0)
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Union of two partials; on equal maxima the lower index wins, so folding partials in any
+// fixed order gives the first occurrence of the maximum.
+__device__ __forceinline__ TopState merge(TopState x, TopState y) {
+  TopState r;
+  r.m = fmaxf(x.m, y.m);
+  const float sx = x.m == -INFINITY ? 0.f : x.s * fast_exp2((x.m - r.m) * LOG2E);
+  const float sy = y.m == -INFINITY ? 0.f : y.s * fast_exp2((y.m - r.m) * LOG2E);
+  r.s = sx + sy;
+  r.arg = x.m > y.m ? x.arg : (y.m > x.m ? y.arg : min(x.arg, y.arg));
+  return r;
+}

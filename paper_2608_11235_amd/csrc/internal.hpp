@@ -82,6 +82,30 @@ hipError_t launch_gemm(int epi, const GemmArgs& a, const GemmPlan& p, hipStream_
 hipError_t launch_qkv_finish(const float* part, int splits, int M, int N, const float* bias,
                              const QkvOut& o, hipStream_t s);
 
+// ---- LM head for few rows (M <= 64) ------------------------------------------------------
+struct LmHeadArgs {
+  const uint16_t* A; int64_t lda;  // [M, K] normalised rows
+  const uint16_t* Wp;              // vocab projection [N, K] in the packed layout
+  int M, N, K;
+  float scale;                     // logit scale, applied before the bf16 rounding
+  uint16_t* logits; int64_t ldc;   // logits mode: [M, N] bf16
+  // top-1 mode: per row, partial statistics of each 128-entry vocab range ([M][n_parts])
+  float* part_m; float* part_s; int* part_arg;
+  int n_parts;                     // set by launch_lm_head
+  int mask_id;                     // left out of the top-1 statistics
+};
+constexpr int LM_HEAD_FUSED_MAX_ROWS = 64;
+int lm_head_parts(int N);
+// packed copy of the vocab projection (written once, read by launch_lm_head)
+size_t lm_head_packed_elems(int N, int K);
+hipError_t launch_pack_lm_head(const uint16_t* W, uint16_t* packed, int N, int K, hipStream_t s);
+bool lm_head_supported(int M, int N, int K, int64_t lda);
+hipError_t launch_lm_head(const LmHeadArgs& a, bool top1, hipStream_t s);
+// rows are scored like launch_vocab_top1: row r of batch row b (n_rows per batch row) goes to
+// top1/conf[b * out_ld + out_off + r]
+hipError_t launch_top1_merge(const LmHeadArgs& a, int n_rows, int out_ld, int out_off,
+                             int32_t* top1, float* conf, hipStream_t s);
+
 // ---- attention ---------------------------------------------------------------------------
 hipError_t launch_attention(const uint16_t* q, const uint16_t* k, const uint16_t* vt,
                             uint16_t* out, int B, int L, int Ls, int H, int Hkv, int hd,

@@ -54,6 +54,8 @@ struct cora_model {
   size_t weight_bytes = 0, ws_bytes = 0;
 
   uint16_t *embed = nullptr, *lm_head = nullptr;
+  // LM head in the packed layout of the few-row kernel (null when the shape does not fit it)
+  uint16_t* lm_head_packed = nullptr;
   float* ones = nullptr;  // all norm weights are 1
   struct Layer {
     uint16_t *wqkv, *wo, *wgu, *wd;
@@ -69,6 +71,9 @@ struct cora_model {
   int num_cus = 256;
   float* splitk_ws = nullptr;
   size_t splitk_ws_floats = 0;
+  // per-row partial softmax statistics of the fused LM head ([64][lm_head_parts(V)])
+  float *lmh_pm = nullptr, *lmh_ps = nullptr;
+  int* lmh_pa = nullptr;
   // decode state owned for cora_block_decode
   int32_t *s_tokens = nullptr, *s_prev = nullptr, *s_persist = nullptr, *s_block = nullptr;
   int32_t *s_step = nullptr, *s_top1 = nullptr, *s_done = nullptr, *s_passes = nullptr;
@@ -141,6 +146,9 @@ extern "C" cora_status cora_model_create(const cora_model_cfg* cfg, uint64_t see
 
   // ---- weights
   size_t wb = 2 * align_up((size_t)V * d * 2) + align_up((size_t)d * 4);
+  // packed LM-head copy for steps that score at most 64 rows (one extra V x d matrix)
+  const bool pack_lm = lm_head_supported(1, V, d, d);
+  if (pack_lm) wb += align_up(lm_head_packed_elems(V, d) * 2);
   const size_t per_layer = align_up((size_t)m->qkv_n * d * 2) + align_up((size_t)d * m->hq * 2) +
                            align_up((size_t)2 * m->f_pad * d * 2) +
                            align_up((size_t)d * m->f_pad * 2) +
@@ -159,7 +167,8 @@ extern "C" cora_status cora_model_create(const cora_model_cfg* cfg, uint64_t see
       m->num_cus = cus;
   }
   const size_t skw = gemm_ws_floats_bound(m->num_cus);
-  size_t wsb = align_up(skw * 4) + align_up(M * d * 4) + align_up(M * (size_t)(d > m->hq ? d : m->hq) * 2) +
+  const size_t lmh_parts = (size_t)LM_HEAD_FUSED_MAX_ROWS * lm_head_parts(V);
+  size_t wsb = 3 * align_up(lmh_parts * 4) + align_up(skw * 4) + align_up(M * d * 4) + align_up(M * (size_t)(d > m->hq ? d : m->hq) * 2) +
                align_up(Ms * m->hq * 2) + 2 * align_up(Ms * m->hkv * 2) +
                align_up(M * m->hq * 2) + align_up(M * m->f_pad * 2) + align_up(rows * V * 2) +
                2 * align_up((size_t)m->max_seq_pad * (hd / 2) * 4) +
@@ -184,6 +193,7 @@ extern "C" cora_status cora_model_create(const cora_model_cfg* cfg, uint64_t see
   Arena w{(char*)m->weight_mem, 0, wb};
   m->embed = w.take<uint16_t>((size_t)V * d);
   m->lm_head = w.take<uint16_t>((size_t)V * d);
+  if (pack_lm) m->lm_head_packed = w.take<uint16_t>(lm_head_packed_elems(V, d));
   m->ones = w.take<float>(d);
   m->layers.resize(L_);
   for (auto& ly : m->layers) {
@@ -194,6 +204,9 @@ extern "C" cora_status cora_model_create(const cora_model_cfg* cfg, uint64_t see
     ly.bqkv = cfg->qkv_bias ? w.take<float>(m->qkv_n) : nullptr;
   }
   Arena a{(char*)m->ws_mem, 0, wsb};
+  m->lmh_pm = a.take<float>(lmh_parts);
+  m->lmh_ps = a.take<float>(lmh_parts);
+  m->lmh_pa = a.take<int>(lmh_parts);
   m->splitk_ws = a.take<float>(skw);
   m->splitk_ws_floats = skw;
   m->h = a.take<float>(M * d);
@@ -230,6 +243,7 @@ extern "C" cora_status cora_model_create(const cora_model_cfg* cfg, uint64_t see
     HIP_TRY(hipMemsetAsync(m->ws_mem, 0, wsb, s));  // finite zeros in every padding region
     HIP_TRY(launch_init_bf16(m->embed, seed, 1, V, d, d, ROW_IDENTITY, 0, sd, hd, s));
     HIP_TRY(launch_init_bf16(m->lm_head, seed, 2, V, d, d, ROW_IDENTITY, 0, sd, hd, s));
+    if (m->lm_head_packed) HIP_TRY(launch_pack_lm_head(m->lm_head, m->lm_head_packed, V, d, s));
     HIP_TRY(launch_fill_f32(m->ones, 1.0f, d, s));
     for (int l = 0; l < (int)L_; ++l) {
       const auto& ly = m->layers[l];
@@ -413,13 +427,57 @@ static cora_status run_layers(cora_model* m, const int32_t* tokens, int B, int L
   return CORA_OK;
 }
 
+// few rows read the packed weights (HBM-bound stream), more rows take the tiled GEMM
+static bool lm_head_few_rows(const cora_model* m, int n_out_rows) {
+  return m->lm_head_packed && n_out_rows <= LM_HEAD_FUSED_MAX_ROWS &&
+         lm_head_supported(n_out_rows, m->cfg.vocab, m->cfg.d_model, m->cfg.d_model);
+}
+
+static LmHeadArgs lm_args(const cora_model* m, int n_out_rows) {
+  const auto& c = m->cfg;
+  LmHeadArgs a{};
+  a.A = m->a; a.lda = c.d_model; a.Wp = m->lm_head_packed;
+  a.M = n_out_rows; a.N = c.vocab; a.K = c.d_model; a.scale = c.logit_scale;
+  a.part_m = m->lmh_pm; a.part_s = m->lmh_ps; a.part_arg = m->lmh_pa;
+  a.mask_id = c.mask_id;
+  return a;
+}
+
 static cora_status lm_head(cora_model* m, const RowSel& sel, int n_out_rows, uint16_t* logits,
                            hipStream_t s) {
   const auto& c = m->cfg;
   HIP_TRY(launch_rmsnorm(m->h, m->ones, m->a, n_out_rows, c.d_model, c.rms_eps, sel, s));
+  if (lm_head_few_rows(m, n_out_rows)) {
+    LmHeadArgs a = lm_args(m, n_out_rows);
+    a.logits = logits;
+    a.ldc = c.vocab;
+    HIP_TRY(launch_lm_head(a, false, s));
+    return CORA_OK;
+  }
   GemmArgs g{m->a, c.d_model, m->lm_head, c.d_model, n_out_rows, c.vocab, c.d_model, logits,
              c.vocab, nullptr, c.logit_scale};
   return gemm(m, EPI_BF16, g, s);
+}
+
+// Scores of the selected rows (Eq. 1) into top1/conf[b * out_ld + out_off + r]: fused into
+// the LM-head pass for few rows (no logits written), else logits then the row reduction.
+static cora_status score_rows(cora_model* m, const RowSel& sel, int B, int n_rows,
+                              const VocabGateArgs& vg, hipStream_t s) {
+  const auto& c = m->cfg;
+  const int M = B * n_rows;
+  if (lm_head_few_rows(m, M)) {
+    HIP_TRY(launch_rmsnorm(m->h, m->ones, m->a, M, c.d_model, c.rms_eps, sel, s));
+    const LmHeadArgs a = lm_args(m, M);
+    HIP_TRY(launch_lm_head(a, true, s));
+    HIP_TRY(launch_top1_merge(a, n_rows, vg.out_ld, vg.out_off, vg.top1, vg.conf, s));
+    return CORA_OK;
+  }
+  if (cora_status e = lm_head(m, sel, M, m->logits, s)) return e;
+  VocabGateArgs r = vg;
+  r.logits = m->logits;
+  r.n_rows = n_rows;
+  HIP_TRY(launch_vocab_top1(r, s));
+  return CORA_OK;
 }
 
 extern "C" cora_status cora_forward_logits(cora_model* m, const int32_t* d_tokens, int32_t B,
@@ -525,20 +583,17 @@ static cora_status denoise_step(cora_model* m, cora_state* st, const cora_sched_
     for (int r0 = 0; r0 < G; r0 += m->max_rows) {
       const int n = G - r0 < m->max_rows ? G - r0 : m->max_rows;
       const RowSel sel{1, L, n, st->prompt_len + r0, 0, 0, 0, nullptr};
-      if (cora_status e = lm_head(m, sel, B * n, m->logits, s)) return e;
       VocabGateArgs c = a;
-      c.n_rows = n;
       c.out_off = r0;
-      HIP_TRY(launch_vocab_top1(c, s));
+      if (cora_status e = score_rows(m, sel, B, n, c, s)) return e;
     }
     HIP_TRY(launch_gate_rules(a, s));
     return CORA_OK;
   }
   const RowSel sel{2, L, blk, 0, st->prompt_len, blk, st->gen_len / blk, st->block_idx};
-  if (cora_status e = lm_head(m, sel, B * blk, m->logits, s)) return e;
   const VocabGateArgs a = vg_args(m->logits, blk, -1, m->cfg.vocab, m->cfg.mask_id, st, -1, sc,
                                   gt);
-  HIP_TRY(launch_vocab_top1(a, s));
+  if (cora_status e = score_rows(m, sel, B, blk, a, s)) return e;
   HIP_TRY(launch_gate_rules(a, s));
   return CORA_OK;
 }

@@ -28,30 +28,10 @@
 
 namespace cora {
 
-struct TopState {
-  float m, s;
-  int arg;  // during the row loop (VEC): index of the chunk that first reached m
-};
 // raw words of the chunk that first reached the running max (VEC row loop)
 struct BestChunk {
   uint32_t w0, w1, w2, w3;
 };
-
-constexpr float LOG2E = 1.4426950408889634f;
-
-// 2^x with the hardware v_exp_f32: results below 2^-126 flush to zero, which cannot change
-// a softmax sum that already holds the max term (1.0)
-__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
-
-__device__ __forceinline__ TopState merge(TopState x, TopState y) {
-  TopState r;
-  r.m = fmaxf(x.m, y.m);
-  const float sx = x.m == -INFINITY ? 0.f : x.s * fast_exp2((x.m - r.m) * LOG2E);
-  const float sy = y.m == -INFINITY ? 0.f : y.s * fast_exp2((y.m - r.m) * LOG2E);
-  r.s = sx + sy;
-  r.arg = x.m > y.m ? x.arg : (y.m > x.m ? y.arg : min(x.arg, y.arg));
-  return r;
-}
 
 // Running (max, sum of exp(l - max)) over a group of 32 logits (chunks i = 0..3 of 8): one
 // max and one rescale per group, then exp2 of every logit relative to the running max.  The
@@ -95,7 +75,7 @@ __global__ __launch_bounds__(256) void k_vocab_top1(VocabGateArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const uint16_t* x = a.logits + (int64_t)row * a.V;
 
-  TopState t{-INFINITY, 0.f, INT_MAX};
+  TopState t{-INFINITY, 0.f, INT_MAX};  // VEC: t.arg is a chunk index until the row ends
   if constexpr (VEC) {
     // Thread tid reads chunks (16 bytes = 8 logits) tid + 256 i, in groups of 4: chunks
     // c, c + 256, c + 512, c + 768.  The next group's loads are in flight while the current

@@ -62,10 +62,10 @@ def _check_logits(spec, B, L, row_begin, n_rows, seed=0, tag=""):
     return err, ref
 
 
-@pytest.mark.parametrize("n_rows", [1, 33, 70])
+@pytest.mark.parametrize("n_rows", [1, 20, 32, 33, 70])
 def test_lm_head_only(n_rows):
-    """0 layers: embedding -> final RMSNorm -> LM head (the GEMM's small- and large-M paths,
-    a ragged vocab tail)."""
+    """0 layers: embedding -> final RMSNorm -> LM head: the few-row kernel at B * n_rows <= 64
+    (both of its row-block widths), the tiled GEMM above, and a ragged vocab tail."""
     require_gpu()
     spec = si.ModelSpec("lmhead", 0, 192, 3, 3, 64, 64, 1000, 7, False, 1e-5, 1e4, 4.0)
     _check_logits(spec, 2, 80, 3, n_rows)
