@@ -8,38 +8,47 @@ namespace cora {
 
 // One workgroup per row: fold the split-K partials of a residual GEMM into h (in split
 // order, so the sum does not depend on scheduling), then normalise the updated row for the
-// next GEMM.  Row values stay in registers between the two phases.
+// next GEMM.  Row values stay in registers between the two phases.  SPLITS and the chunk
+// count C (float4 chunks per thread, C * 1024 >= d) are compile-time, so every partial and
+// residual load of a thread is issued before the first add.
+template <int SPLITS, int C>
 __global__ __launch_bounds__(256) void k_residual_norm(float* __restrict__ h,
                                                        const float* __restrict__ part,
-                                                       int splits, int64_t slab, int d,
+                                                       int64_t slab, int d,
                                                        const float* __restrict__ w,
                                                        uint16_t* __restrict__ out, float eps) {
-  constexpr int MAXC = RESIDUAL_NORM_MAX_D / 1024;  // float4 chunks per thread
   const int64_t r = blockIdx.x;
   float* x = h + r * d;
   const float* p = part + r * d;
-  float4 v[MAXC];
-  float ss = 0.f;
+  float4 pv[C][SPLITS], v[C];
 #pragma unroll
-  for (int i = 0; i < MAXC; ++i) {
+  for (int i = 0; i < C; ++i) {
     const int c = (threadIdx.x + i * 256) * 4;
     if (c < d) {
-      float4 acc = *reinterpret_cast<const float4*>(p + c);
-      for (int sp = 1; sp < splits; ++sp) {
-        const float4 q = *reinterpret_cast<const float4*>(p + sp * slab + c);
-        acc.x += q.x;
-        acc.y += q.y;
-        acc.z += q.z;
-        acc.w += q.w;
+#pragma unroll
+      for (int sp = 0; sp < SPLITS; ++sp) pv[i][sp] = *reinterpret_cast<const float4*>(p + sp * slab + c);
+      v[i] = *reinterpret_cast<const float4*>(x + c);
+    }
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < C; ++i) {
+    const int c = (threadIdx.x + i * 256) * 4;
+    if (c < d) {
+      float4 acc = pv[i][0];
+#pragma unroll
+      for (int sp = 1; sp < SPLITS; ++sp) {
+        acc.x += pv[i][sp].x;
+        acc.y += pv[i][sp].y;
+        acc.z += pv[i][sp].z;
+        acc.w += pv[i][sp].w;
       }
-      float4 hv = *reinterpret_cast<const float4*>(x + c);
-      hv.x += acc.x;
-      hv.y += acc.y;
-      hv.z += acc.z;
-      hv.w += acc.w;
-      *reinterpret_cast<float4*>(x + c) = hv;
-      v[i] = hv;
-      ss += hv.x * hv.x + hv.y * hv.y + hv.z * hv.z + hv.w * hv.w;
+      v[i].x += acc.x;
+      v[i].y += acc.y;
+      v[i].z += acc.z;
+      v[i].w += acc.w;
+      *reinterpret_cast<float4*>(x + c) = v[i];
+      ss += v[i].x * v[i].x + v[i].y * v[i].y + v[i].z * v[i].z + v[i].w * v[i].w;
     }
   }
   if (!out) return;
@@ -51,7 +60,7 @@ __global__ __launch_bounds__(256) void k_residual_norm(float* __restrict__ h,
   const float inv = 1.0f / sqrtf(tot / (float)d + eps);
   uint16_t* o = out + r * d;
 #pragma unroll
-  for (int i = 0; i < MAXC; ++i) {
+  for (int i = 0; i < C; ++i) {
     const int c = (threadIdx.x + i * 256) * 4;
     if (c < d) {
       const float4 g = *reinterpret_cast<const float4*>(w + c);
@@ -63,23 +72,44 @@ __global__ __launch_bounds__(256) void k_residual_norm(float* __restrict__ h,
   }
 }
 
+template <int SPLITS>
+static void residual_norm_c(int C, dim3 grid, hipStream_t s, float* h, const float* part,
+                            int64_t slab, int d, const float* w, uint16_t* out, float eps) {
+#define RN(C_) hipLaunchKernelGGL((k_residual_norm<SPLITS, C_>), grid, dim3(256), 0, s, h, part, slab, d, w, out, eps)
+  if (C <= 1) RN(1);
+  else if (C <= 2) RN(2);
+  else if (C <= 4) RN(4);
+  else RN(8);
+#undef RN
+}
+
 hipError_t launch_residual_norm(float* h, const float* part, int splits, int rows, int d,
                                 const float* w, uint16_t* out, float eps, hipStream_t s) {
   if (rows == 0) return hipSuccess;
-  if (splits < 1 || d % 4 != 0 || d > RESIDUAL_NORM_MAX_D) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_residual_norm, dim3(rows), dim3(256), 0, s, h, part, splits,
-                     (int64_t)rows * d, d, w, out, eps);
+  if (d % 4 != 0 || d > RESIDUAL_NORM_MAX_D) return hipErrorInvalidValue;
+  static_assert(RESIDUAL_NORM_MAX_D <= 8 * 1024, "at most 8 float4 chunks per thread");
+  const int C = (d + 1023) / 1024;
+  const int64_t slab = (int64_t)rows * d;
+  const dim3 grid(rows);
+  switch (splits) {
+    case 1: residual_norm_c<1>(C, grid, s, h, part, slab, d, w, out, eps); break;
+    case 2: residual_norm_c<2>(C, grid, s, h, part, slab, d, w, out, eps); break;
+    case 4: residual_norm_c<4>(C, grid, s, h, part, slab, d, w, out, eps); break;
+    case 8: residual_norm_c<8>(C, grid, s, h, part, slab, d, w, out, eps); break;
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 
 // QKV projection partials -> q and k with rotate-half RoPE, v transposed.  q/k columns are
-// pair-interleaved within a head, so a thread's column pair (2x, 2x+1) is exactly one RoPE
-// pair; it handles the rows 4y .. 4y+3, and for v writes the 4 positions as one vector when
-// they fall in one sequence.
-__global__ __launch_bounds__(256) void k_qkv_finish(const float* __restrict__ part, int splits,
-                                                    int M, int N, const float* __restrict__ bias,
-                                                    QkvOut o) {
-  const int c = (blockIdx.x * 256 + threadIdx.x) * 2;
+// pair-interleaved within a head, so a thread's 4 columns (4x .. 4x+3, inside one head) are
+// two RoPE pairs; it handles the rows 4y .. 4y+3 (all 16-byte partial loads issued before
+// the first add), and for v writes each column's 4 positions as one vector when they fall in
+// one sequence.
+template <int SPLITS>
+__global__ __launch_bounds__(256) void k_qkv_finish(const float* __restrict__ part, int M, int N,
+                                                    const float* __restrict__ bias, QkvOut o) {
+  const int c = (blockIdx.x * 256 + threadIdx.x) * 4;
   if (c >= N) return;
   const int r0 = blockIdx.y * 4;
   const int nr = M - r0 < 4 ? M - r0 : 4;
@@ -89,47 +119,60 @@ __global__ __launch_bounds__(256) void k_qkv_finish(const float* __restrict__ pa
   const int sec = c < hq ? 0 : (c < hq + hkv ? 1 : 2);
   const int cc = c - (sec == 0 ? 0 : (sec == 1 ? hq : hq + hkv));
   const int head = cc / hd, pd = cc % hd;
-  const float b0 = bias ? bias[c] : 0.f, b1 = bias ? bias[c + 1] : 0.f;
-  float x0[4], x1[4];
+  const float4 bv = bias ? *reinterpret_cast<const float4*>(bias + c) : float4{0.f, 0.f, 0.f, 0.f};
+  float4 pv[4][SPLITS];
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+    if (t < nr) {
+#pragma unroll
+      for (int sp = 0; sp < SPLITS; ++sp)
+        pv[t][sp] = *reinterpret_cast<const float4*>(part + sp * slab + (int64_t)(r0 + t) * N + c);
+    }
+  float x[4][4] = {};  // [row][column]; rows past M stay zero and are not stored
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
-    if (t < nr) {
-      const float* p = part + (int64_t)(r0 + t) * N + c;
-      float2 v = *reinterpret_cast<const float2*>(p);
-      for (int sp = 1; sp < splits; ++sp) {
-        const float2 q = *reinterpret_cast<const float2*>(p + sp * slab);
-        v.x += q.x;
-        v.y += q.y;
-      }
-      x0[t] = v.x + b0;
-      x1[t] = v.y + b1;
+    if (t >= nr) continue;
+    float4 v = pv[t][0];
+#pragma unroll
+    for (int sp = 1; sp < SPLITS; ++sp) {
+      v.x += pv[t][sp].x;
+      v.y += pv[t][sp].y;
+      v.z += pv[t][sp].z;
+      v.w += pv[t][sp].w;
     }
+    x[t][0] = v.x + bv.x;
+    x[t][1] = v.y + bv.y;
+    x[t][2] = v.z + bv.z;
+    x[t][3] = v.w + bv.w;
   }
   int b = r0 / o.L, pos = r0 - b * o.L;
   if (sec == 2 && nr == 4 && (o.L & 3) == 0) {  // pos % 4 == 0: all four rows in sequence b
     uint16_t* dst = o.vt + ((int64_t)(b * o.n_kv_heads + head) * hd + pd) * o.Ls + pos;
-    u32x2_t v0, v1;
-    v0.x = pack_bf16x2(x0[0], x0[1]);
-    v0.y = pack_bf16x2(x0[2], x0[3]);
-    v1.x = pack_bf16x2(x1[0], x1[1]);
-    v1.y = pack_bf16x2(x1[2], x1[3]);
-    *reinterpret_cast<u32x2_t*>(dst) = v0;
-    *reinterpret_cast<u32x2_t*>(dst + o.Ls) = v1;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      u32x2_t q;
+      q.x = pack_bf16x2(x[0][j], x[1][j]);
+      q.y = pack_bf16x2(x[2][j], x[3][j]);
+      *reinterpret_cast<u32x2_t*>(dst + j * o.Ls) = q;
+    }
     return;
   }
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
     if (t >= nr) break;
     if (sec < 2) {
-      const float cs = o.cos_t[pos * half + (pd >> 1)], sn = o.sin_t[pos * half + (pd >> 1)];
-      const float y0 = x0[t] * cs - x1[t] * sn, y1 = x1[t] * cs + x0[t] * sn;
+      const float2 cs = *reinterpret_cast<const float2*>(o.cos_t + pos * half + (pd >> 1));
+      const float2 sn = *reinterpret_cast<const float2*>(o.sin_t + pos * half + (pd >> 1));
+      u32x2_t q;
+      q.x = pack_bf16x2(x[t][0] * cs.x - x[t][1] * sn.x, x[t][1] * cs.x + x[t][0] * sn.x);
+      q.y = pack_bf16x2(x[t][2] * cs.y - x[t][3] * sn.y, x[t][3] * cs.y + x[t][2] * sn.y);
       uint16_t* dst = sec == 0 ? o.q + ((int64_t)(b * o.n_heads + head) * o.Ls + pos) * hd
                                : o.k + ((int64_t)(b * o.n_kv_heads + head) * o.Ls + pos) * hd;
-      *reinterpret_cast<uint32_t*>(dst + pd) = pack_bf16x2(y0, y1);
+      *reinterpret_cast<u32x2_t*>(dst + pd) = q;
     } else {
       uint16_t* dst = o.vt + ((int64_t)(b * o.n_kv_heads + head) * hd + pd) * o.Ls + pos;
-      dst[0] = (uint16_t)f32_to_bf16_bits(x0[t]);
-      dst[o.Ls] = (uint16_t)f32_to_bf16_bits(x1[t]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) dst[j * o.Ls] = (uint16_t)f32_to_bf16_bits(x[t][j]);
     }
     if (++pos == o.L) {
       pos = 0;
@@ -141,9 +184,17 @@ __global__ __launch_bounds__(256) void k_qkv_finish(const float* __restrict__ pa
 hipError_t launch_qkv_finish(const float* part, int splits, int M, int N, const float* bias,
                              const QkvOut& o, hipStream_t s) {
   if (M == 0) return hipSuccess;
-  if (splits < 1 || N % 2 != 0 || o.head_dim % 2 != 0) return hipErrorInvalidValue;
-  const dim3 grid((N / 2 + 255) / 256, (M + 3) / 4);
-  hipLaunchKernelGGL(k_qkv_finish, grid, dim3(256), 0, s, part, splits, M, N, bias, o);
+  if (N % 4 != 0 || o.head_dim % 4 != 0) return hipErrorInvalidValue;
+  const dim3 grid((N / 4 + 255) / 256, (M + 3) / 4);
+#define QF(S_) hipLaunchKernelGGL((k_qkv_finish<S_>), grid, dim3(256), 0, s, part, M, N, bias, o)
+  switch (splits) {
+    case 1: QF(1); break;
+    case 2: QF(2); break;
+    case 4: QF(4); break;
+    case 8: QF(8); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef QF
   return hipGetLastError();
 }
 
