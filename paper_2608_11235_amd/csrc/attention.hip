@@ -9,13 +9,15 @@
 // use SPLIT = 2, which doubles the wavefronts per SIMD and halves each one's serial chain.
 // Key tiles of 64 are staged in LDS, double buffered: the next tile's loads are in flight
 // in registers while the current tile is multiplied out of LDS (one barrier per tile).
+// Softmax terms use the hardware v_exp_f32 (arguments <= 0; results below 2^-126 flush to
+// zero, which no sum holding its max term can notice).
 // Everything is computed transposed with v_mfma_f32_16x16x32_bf16 so that a query's
 // softmax statistics never leave its lanes:
 //   S^T = K Q^T   (A = K tile from LDS, B = Q^T held in registers)
 //   O^T = V^T P^T (A = V^T tile from LDS, B = P^T straight from the S^T registers)
-// In S^T a lane holds keys 16kb + 4(lane/16) + i of query lane%16; feeding those
-// registers as P^T fixes the key order of one 32-key MFMA step, and the V^T fragment
-// is read from LDS in that same order.
+// Feeding the S^T registers as P^T fixes the key order of a 32-key MFMA step; the K tile's
+// rows are stored in a permuted key order (see krow) so that this order is 8 consecutive
+// keys per lane group, and each V^T fragment is a single 16-byte LDS read.
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -56,31 +58,42 @@ __global__ __launch_bounds__(256 * SPLIT) void k_attention(const uint16_t* __res
   float m_run = -INFINITY, l_part = 0.f;
 
   // K tile [64 keys][HD] and V^T tile [HD][64 keys] of part tpart: chunk c of this thread
+  // (pointers of key 0; a tile adds the uniform key0 * HD / key0)
   u32x4_t rk[CK], rv[CK];
+  const uint16_t* kp[CK];
+  const uint16_t* vp[CK];
+#pragma unroll
+  for (int i = 0; i < CK; ++i) {
+    const int c = tl + i * 256;
+    kp[i] = kh + (c / (HD / 8)) * HD + (c % (HD / 8)) * 8;
+    vp[i] = vh + (int64_t)(c / (KT / 8)) * Ls + (c % (KT / 8)) * 8;
+  }
   auto fetch = [&](int key0) {
 #pragma unroll
     for (int i = 0; i < CK; ++i) {
-      const int c = tl + i * 256;
-      const int kr = c / (HD / 8), kc = (c % (HD / 8)) * 8;
-      rk[i] = *reinterpret_cast<const u32x4_t*>(kh + (int64_t)(key0 + kr) * HD + kc);
-      const int vr = c / (KT / 8), vc = (c % (KT / 8)) * 8;
-      rv[i] = *reinterpret_cast<const u32x4_t*>(vh + (int64_t)vr * Ls + key0 + vc);
+      rk[i] = *reinterpret_cast<const u32x4_t*>(kp[i] + (int64_t)key0 * HD);
+      rv[i] = *reinterpret_cast<const u32x4_t*>(vp[i] + key0);
     }
   };
+  // K rows are stored in a permuted key order: tile key k = 32 a + 8 g + 4 b + i (a, b in
+  // {0, 1}, g < 4, i < 4) goes to LDS row (2 a + b) * 16 + 4 g + i.  S^T block kb then holds,
+  // in lane group g, keys 32 (kb / 2) + 8 g + 4 (kb % 2) + i, so the 8 P^T slots of lane
+  // group g in key step ks are the 8 consecutive keys 32 ks + 8 g .. + 7 and the matching
+  // V^T fragment is one 16-byte read of the natural V^T layout.
+  auto krow = [](int k) { return ((k >> 5) * 2 + ((k >> 2) & 1)) * 16 + ((k >> 3) & 3) * 4 + (k & 3); };
   auto stash = [&](int buf) {
 #pragma unroll
     for (int i = 0; i < CK; ++i) {
       const int c = tl + i * 256;
       const int kr = c / (HD / 8), kc = (c % (HD / 8)) * 8;
-      *reinterpret_cast<u32x4_t*>(&Ks[buf][tpart][kr * LDKS + kc]) = rk[i];
+      *reinterpret_cast<u32x4_t*>(&Ks[buf][tpart][krow(kr) * LDKS + kc]) = rk[i];
       const int vr = c / (KT / 8), vc = (c % (KT / 8)) * 8;
       *reinterpret_cast<u32x4_t*>(&Vs[buf][tpart][vr * LDVS + vc]) = rv[i];
     }
   };
 
-  // part p owns key tiles [p * per, min((p + 1) * per, n_tiles)); iteration j works on
-  // tile p * per + j of every part, and parts that ran out skip the work but keep the
-  // barriers
+  // part p owns key tiles [p * per, min((p + 1) * per, n_tiles)); step j works on tile
+  // p * per + j of every part, and parts that ran out skip the work but keep the barriers.
   const int n_tiles = (L + KT - 1) / KT;
   const int per = (n_tiles + SPLIT - 1) / SPLIT;
   const bool load0 = tpart * per < n_tiles;
@@ -104,19 +117,29 @@ __global__ __launch_bounds__(256 * SPLIT) void k_attention(const uint16_t* __res
         }
       }
       float tmax = -INFINITY;
+      if (key0 + KT <= L) {  // whole tile inside the sequence (uniform)
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
+        for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int key = key0 + kb * 16 + g * 4 + i;
-          const float v = key < L ? st[kb][i] * scale_log2 : -INFINITY;
-          st[kb][i] = v;
-          tmax = fmaxf(tmax, v);
-        }
+          for (int i = 0; i < 4; ++i) {
+            st[kb][i] *= scale_log2;
+            tmax = fmaxf(tmax, st[kb][i]);
+          }
+      } else {
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int key = key0 + 32 * (kb >> 1) + 8 * g + 4 * (kb & 1) + i;
+            const float v = key < L ? st[kb][i] * scale_log2 : -INFINITY;
+            st[kb][i] = v;
+            tmax = fmaxf(tmax, v);
+          }
+      }
       tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
       tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
       const float m_new = fmaxf(m_run, tmax);
-      const float alpha = exp2f(m_run - m_new);
+      const float alpha = fast_exp2(m_run - m_new);  // 0 while m_run is -inf
       m_run = m_new;
       l_part *= alpha;
 #pragma unroll
@@ -125,7 +148,7 @@ __global__ __launch_bounds__(256 * SPLIT) void k_attention(const uint16_t* __res
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const float p = exp2f(st[kb][i] - m_new);
+          const float p = fast_exp2(st[kb][i] - m_new);
           st[kb][i] = p;
           l_part += p;
         }
@@ -139,10 +162,8 @@ __global__ __launch_bounds__(256 * SPLIT) void k_attention(const uint16_t* __res
         const bf16x8_t bfrag = as_bf16x8(pb);
 #pragma unroll
         for (int d = 0; d < HD / 16; ++d) {
-          const uint16_t* vrow = &Vs[buf][part][(d * 16 + r16) * LDVS + ks * 32 + g * 4];
-          const u32x2_t lo = *reinterpret_cast<const u32x2_t*>(vrow);
-          const u32x2_t hi = *reinterpret_cast<const u32x2_t*>(vrow + 16);
-          const u32x4_t av = u32x4_t{lo.x, lo.y, hi.x, hi.y};
+          const u32x4_t av = *reinterpret_cast<const u32x4_t*>(
+              &Vs[buf][part][(d * 16 + r16) * LDVS + ks * 32 + g * 8]);
           o[d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(av), bfrag, o[d], 0, 0, 0);
         }
       }
@@ -170,7 +191,7 @@ __global__ __launch_bounds__(256 * SPLIT) void k_attention(const uint16_t* __res
     if (part == 1) return;
     const float m1 = comb[slot], l1 = comb[slot + 64];
     const float m = fmaxf(m_run, m1);
-    const float a0 = exp2f(m_run - m), a1 = exp2f(m1 - m);
+    const float a0 = fast_exp2(m_run - m), a1 = fast_exp2(m1 - m);
     l_part = l_part * a0 + l1 * a1;
 #pragma unroll
     for (int d = 0; d < HD / 16; ++d)
