@@ -221,6 +221,51 @@ def gated_decode_leg(logit_scale=8.0):
     return out
 
 
+def compaction_leg(batch=8, logit_scale=8.0):
+    """Labelled batch-row compaction run (not a paper configuration): 8 prompts at the
+    LLaDA-8B shape with logits x8, so rows accept tokens at different rates and finish at
+    different passes.  The same gated block decode is timed with compaction on (finished
+    rows leave the dense pass) and off (every row runs until the last one finishes).  At
+    this shape the GEMM split-K and tile plans depend on the row count, so the two decodes
+    round differently and, with random weights, part ways; tokens_equal reports that."""
+    from dataclasses import replace
+
+    import numpy as np
+    import torch
+
+    import seeded_inputs as si
+    from paper_2608_11235_amd import LLADA_8B, Gate, Model, Sched
+
+    spec = replace(LLADA_8B, logit_scale=logit_scale, name=f"llada8b-logits-x{logit_scale:g}")
+    prompt = torch.from_numpy(si.prompt_tokens(3, batch, P, spec.vocab, spec.mask_id)).cuda()
+    sched, gate = Sched(BLK, S), Gate(DELTA_P, M_REQ, True)
+    out = {"label": f"LLaDA-8B shape, B={batch}, logits x{logit_scale:g} so the gate fires on "
+                    "random weights; not a paper configuration", "gate": [DELTA_P, M_REQ]}
+    with Model(spec, seed=0, max_batch=batch, max_seq=P + G) as m:
+        m.block_decode(prompt, BLK, sched, gate)  # warm-up: one block
+        res = {}
+        for name, on in (("off", False), ("on", True)):
+            m.set_compaction(on)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            y, passes, total = m.block_decode(prompt, G, sched, gate)
+            torch.cuda.synchronize()
+            dt = time.perf_counter() - t0
+            res[name] = (y.cpu().numpy(), passes, total, dt)
+    rows = res["on"][1].sum(axis=1)
+    out.update({
+        "batch_passes": res["on"][2],
+        "row_passes": [int(v) for v in rows],
+        "row_passes_computed_on": int(rows.sum()),
+        "row_passes_computed_off": int(res["off"][2] * batch),
+        "decode_s_off": round(res["off"][3], 3), "decode_s_on": round(res["on"][3], 3),
+        "speedup": round(res["off"][3] / res["on"][3], 3),
+        "tokens_equal": bool((res["on"][0] == res["off"][0]).all()),
+        "passes_equal": bool((res["on"][1] == res["off"][1]).all()),
+    })
+    return out
+
+
 def copy_calibration(nbytes=1 << 30, iters=5):
     """A plain device-to-device copy of known size: reference for HBM byte counters."""
     import torch
@@ -250,7 +295,10 @@ def main():
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-gated", action="store_true",
                     help="skip the labelled logits-x8 gated-decode leg")
-    ap.add_argument("--only", choices=["all", "pass", "vocab", "copy", "gated"], default="all",
+    ap.add_argument("--no-compaction", action="store_true",
+                    help="skip the labelled B=8 batch-row compaction leg")
+    ap.add_argument("--only", choices=["all", "pass", "vocab", "copy", "gated", "compaction"],
+                    default="all",
                     help="run one leg only (profiling runs): the timed passes, the vocab/gate "
                          "kernel, or a plain 1 GiB device copy that calibrates byte counters")
     args = ap.parse_args()
@@ -263,8 +311,12 @@ def main():
     if args.only == "gated":
         print(json.dumps({"gated_decode_logits_x8": gated_decode_leg()}), flush=True)
         return
+    if args.only == "compaction":
+        print(json.dumps({"compaction_b8_logits_x8": compaction_leg()}), flush=True)
+        return
     if args.only == "pass":
         args.no_decode = args.no_vocab = args.no_cpu_baseline = args.no_gated = True
+        args.no_compaction = True
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (batch rows "
               "decode independently, so more GPUs shard rows with no collective)", file=sys.stderr)
@@ -357,6 +409,8 @@ def main():
         result["vocab_gate_roofline"] = vocab_gate_roofline()
     if not args.no_gated:
         result["gated_decode_logits_x8"] = gated_decode_leg()
+    if not args.no_compaction:
+        result["compaction_b8_logits_x8"] = compaction_leg()
     if not args.no_cpu_baseline:
         import seeded_inputs as si_
         try:

@@ -193,7 +193,10 @@ cora_status cora_vocab_gate(const uint16_t *d_logits, int32_t n_rows, int32_t ro
 /* Gated block decode of B prompts (d_prompt int32 [B, prompt_len], device):
  * the canvas starts as prompt + gen_len masks, rows decode independently and
  * each block ends once it holds no unresolved position, skipping its
- * remaining passes.  Writes the final canvas to d_out_tokens int32 [B, L]
+ * remaining passes.  With batch-row compaction on (the default, see
+ * cora_model_set_compaction) a row that has finished all its blocks leaves the
+ * dense pass: its final tokens and passes are written out and later passes run
+ * on the live rows only.  Writes the final canvas to d_out_tokens int32 [B, L]
  * (device) and the executed passes per block to h_passes int32
  * [B, gen_len / block_len] (host).  If h_total_passes is not NULL it receives
  * the number of dense passes launched (the batch runs while any row decodes).
@@ -213,6 +216,11 @@ cora_status cora_model_copy_tensor(cora_model *model, int32_t tensor_id, void *h
  * returns the summed event time (ms) and the number of launches since the
  * last reset, waiting for the recorded events. */
 cora_status cora_model_set_timing(cora_model *model, int32_t enable);
+/* Batch-row compaction in cora_block_decode (R15: rows decode independently, so
+ * dropping finished rows from the dense pass changes no live row's inputs; row
+ * results can differ only in rounding where a kernel's split of the work
+ * depends on the row count).  enable != 0 turns it on (default), 0 off. */
+cora_status cora_model_set_compaction(cora_model *model, int32_t enable);
 cora_status cora_model_read_timing(cora_model *model, double *total_ms, int64_t *launches);
 
 /* Device bytes the model holds (weights + workspace). */

@@ -53,6 +53,7 @@ EXPORTS = {
                                   ctypes.POINTER(GateCfg), c_vp, c_vp, c_vp, c_vp]),
     "cora_model_copy_tensor": (c_i32, [c_vp, c_i32, c_vp, c_sz]),
     "cora_model_set_timing": (c_i32, [c_vp, c_i32]),
+    "cora_model_set_compaction": (c_i32, [c_vp, c_i32]),
     "cora_model_read_timing": (c_i32, [c_vp, ctypes.POINTER(c_f64), ctypes.POINTER(ctypes.c_int64)]),
     "cora_model_device_bytes": (c_i32, [c_vp, ctypes.POINTER(c_sz), ctypes.POINTER(c_sz)]),
     "cora_last_error": (ctypes.c_char_p, []),

@@ -169,6 +169,10 @@ class Model:
               "cora_model_copy_tensor")
         return out
 
+    def set_compaction(self, enable: bool):
+        check(_lib.load().cora_model_set_compaction(self._h, int(enable)),
+              "cora_model_set_compaction")
+
     def set_timing(self, enable: bool):
         check(_lib.load().cora_model_set_timing(self._h, int(enable)), "cora_model_set_timing")
 

@@ -41,6 +41,18 @@ hipError_t launch_state_init(const int32_t* prompt, int B, int P, int G, int mas
                              int32_t* tokens, uint8_t* unresolved, int32_t* prev, int32_t* persist,
                              int32_t* block_idx, int32_t* step_idx, int32_t* passes, int n_blocks,
                              hipStream_t s);
+// decode-state rows (device arrays of one state)
+struct DecodeRows {
+  int32_t* tokens; uint8_t* unresolved; int32_t* prev; int32_t* persist;
+  int32_t* block_idx; int32_t* step_idx; int32_t* passes;
+};
+// dst row i <- src row map[i], i < n
+hipError_t launch_gather_state(const DecodeRows& src, const DecodeRows& dst, const int32_t* map,
+                               int n, int L, int n_blocks, hipStream_t s);
+// out_tokens / out_passes row orig[i] <- tokens / passes row rows[i], i < n
+hipError_t launch_scatter_rows(const int32_t* tokens, const int32_t* passes, const int32_t* rows,
+                               const int32_t* orig, int n, int L, int n_blocks,
+                               int32_t* out_tokens, int32_t* out_passes, hipStream_t s);
 
 // ---- GEMM: C[M, N] = A[M, K] . W[N, K]^T, bf16 in, fp32 accumulate ---------------------
 enum GemmEpi { EPI_BF16 = 0, EPI_ADD_F32 = 1, EPI_SWIGLU = 2, EPI_QKV_ROPE = 3, EPI_PART_F32 = 4 };

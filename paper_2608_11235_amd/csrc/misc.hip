@@ -199,4 +199,54 @@ hipError_t launch_state_init(const int32_t* prompt, int B, int P, int G, int mas
   return hipGetLastError();
 }
 
+// ---- batch-row compaction of a decode state ----------------------------------------------
+// dst row i <- src row map[i] (tokens, unresolved, previous top-1, counters, block and step
+// index, passes per block); one workgroup per destination row.
+__global__ void k_gather_state(DecodeRows src, DecodeRows dst, const int32_t* __restrict__ map,
+                               int L, int n_blocks) {
+  const int i = blockIdx.x, r = map[i];
+  const int64_t so = (int64_t)r * L, dof = (int64_t)i * L;
+  for (int e = threadIdx.x; e < L; e += blockDim.x) {
+    dst.tokens[dof + e] = src.tokens[so + e];
+    dst.unresolved[dof + e] = src.unresolved[so + e];
+    dst.prev[dof + e] = src.prev[so + e];
+    dst.persist[dof + e] = src.persist[so + e];
+  }
+  for (int j = threadIdx.x; j < n_blocks; j += blockDim.x)
+    dst.passes[(int64_t)i * n_blocks + j] = src.passes[(int64_t)r * n_blocks + j];
+  if (threadIdx.x == 0) {
+    dst.block_idx[i] = src.block_idx[r];
+    dst.step_idx[i] = src.step_idx[r];
+  }
+}
+
+hipError_t launch_gather_state(const DecodeRows& src, const DecodeRows& dst, const int32_t* map,
+                               int n, int L, int n_blocks, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_gather_state, dim3(n), dim3(256), 0, s, src, dst, map, L, n_blocks);
+  return hipGetLastError();
+}
+
+// Final tokens and passes of the rows rows[i] of a (compacted) state go to row orig[i] of the
+// outputs.
+__global__ void k_scatter_rows(const int32_t* __restrict__ tokens, const int32_t* __restrict__ passes,
+                               const int32_t* __restrict__ rows, const int32_t* __restrict__ orig,
+                               int L, int n_blocks, int32_t* __restrict__ out_tokens,
+                               int32_t* __restrict__ out_passes) {
+  const int r = rows[blockIdx.x], o = orig[blockIdx.x];
+  for (int e = threadIdx.x; e < L; e += blockDim.x)
+    out_tokens[(int64_t)o * L + e] = tokens[(int64_t)r * L + e];
+  for (int j = threadIdx.x; j < n_blocks; j += blockDim.x)
+    out_passes[(int64_t)o * n_blocks + j] = passes[(int64_t)r * n_blocks + j];
+}
+
+hipError_t launch_scatter_rows(const int32_t* tokens, const int32_t* passes, const int32_t* rows,
+                               const int32_t* orig, int n, int L, int n_blocks,
+                               int32_t* out_tokens, int32_t* out_passes, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_scatter_rows, dim3(n), dim3(256), 0, s, tokens, passes, rows, orig, L,
+                     n_blocks, out_tokens, out_passes);
+  return hipGetLastError();
+}
+
 }  // namespace cora

@@ -80,6 +80,14 @@ struct cora_model {
   uint8_t *s_unres = nullptr, *s_decision = nullptr;
   float* s_conf = nullptr;
   int32_t* h_block = nullptr;  // pinned host mirror of block_idx
+  // batch-row compaction: a second state buffer set (live rows are gathered into it once
+  // some rows finish), row maps (pinned host + device, 3 x max_batch), and the per-block
+  // passes of every original row
+  DecodeRows s_alt{};
+  int32_t* h_map = nullptr;
+  int32_t* d_map = nullptr;
+  int32_t* s_final_passes = nullptr;
+  bool compaction = true;
 
   // gate/up GEMM timing
   bool timing = false;
@@ -118,6 +126,7 @@ extern "C" cora_status cora_model_destroy(cora_model* m) {
   if (!m) return CORA_OK;
   for (hipEvent_t e : m->ev) (void)hipEventDestroy(e);
   if (m->h_block) (void)hipHostFree(m->h_block);
+  if (m->h_map) (void)hipHostFree(m->h_map);
   if (m->ws_mem) (void)hipFree(m->ws_mem);
   if (m->weight_mem) (void)hipFree(m->weight_mem);
   delete m;
@@ -174,7 +183,10 @@ extern "C" cora_status cora_model_create(const cora_model_cfg* cfg, uint64_t see
                2 * align_up((size_t)m->max_seq_pad * (hd / 2) * 4) +
                // decode state
                align_up(BL * 4) * 3 + align_up(BL) + align_up(max_batch * 4) * 3 +
-               align_up(BL * 4) * 2 + align_up(rows) + align_up((size_t)max_batch * max_seq * 4);
+               align_up(BL * 4) * 2 + align_up(rows) + align_up((size_t)max_batch * max_seq * 4) +
+               // compaction: second state set, row maps, final passes
+               align_up(BL * 4) * 3 + align_up(BL) + align_up(max_batch * 4) * 2 +
+               align_up((size_t)max_batch * max_seq * 4) * 2 + align_up(3 * max_batch * 4);
   hipError_t e = hipMalloc(&m->weight_mem, wb);
   if (e != hipSuccess) {
     cora_model_destroy(m);
@@ -230,7 +242,18 @@ extern "C" cora_status cora_model_create(const cora_model_cfg* cfg, uint64_t see
   m->s_conf = a.take<float>(BL);
   m->s_decision = a.take<uint8_t>(rows);
   m->s_passes = a.take<int32_t>((size_t)max_batch * max_seq);
+  m->s_alt.tokens = a.take<int32_t>(BL);
+  m->s_alt.prev = a.take<int32_t>(BL);
+  m->s_alt.persist = a.take<int32_t>(BL);
+  m->s_alt.unresolved = a.take<uint8_t>(BL);
+  m->s_alt.block_idx = a.take<int32_t>(max_batch);
+  m->s_alt.step_idx = a.take<int32_t>(max_batch);
+  m->s_alt.passes = a.take<int32_t>((size_t)max_batch * max_seq);
+  m->s_final_passes = a.take<int32_t>((size_t)max_batch * max_seq);
+  m->d_map = a.take<int32_t>((size_t)3 * max_batch);
   e = hipHostMalloc((void**)&m->h_block, max_batch * sizeof(int32_t), hipHostMallocDefault);
+  if (e == hipSuccess)
+    e = hipHostMalloc((void**)&m->h_map, 3 * max_batch * sizeof(int32_t), hipHostMallocDefault);
   if (e != hipSuccess) {
     cora_model_destroy(m);
     return fail(CORA_ERR_HIP, std::string("pinned allocation: ") + hipGetErrorString(e));
@@ -302,6 +325,12 @@ static cora_status grow_events(cora_model* m, size_t n) {
     HIP_TRY(hipEventCreateWithFlags(&e, hipEventDisableSystemFence));
     m->ev.push_back(e);
   }
+  return CORA_OK;
+}
+
+extern "C" cora_status cora_model_set_compaction(cora_model* m, int32_t enable) {
+  if (!m) return fail(CORA_ERR_INVALID_ARG, "null model");
+  m->compaction = enable != 0;
   return CORA_OK;
 }
 
@@ -636,21 +665,59 @@ extern "C" cora_status cora_block_decode(cora_model* m, const int32_t* d_prompt,
                             st.passes, n_blocks, s));
   const int64_t max_passes = (int64_t)n_blocks * sc->steps_per_block;
   int64_t total = 0;
+  // Rows decode independently (the dense pass attends within a row), so once rows finish
+  // their final tokens and passes are written out and the live rows are gathered into the
+  // other state buffer set; later passes run on those rows only.  orig[i] is the caller's
+  // row of compact row i.
+  DecodeRows cur{st.tokens, st.unresolved, st.prev_top1, st.persist, st.block_idx,
+                 st.step_idx, st.passes};
+  DecodeRows alt = m->s_alt;
+  std::vector<int32_t> orig(B);
+  for (int b = 0; b < B; ++b) orig[b] = b;
+  int Bc = B;
+  // final rows of the compact state -> outputs (rows listed in h_map[0, n), originals after)
+  auto write_out = [&](const std::vector<int32_t>& rows) -> cora_status {
+    const int n = (int)rows.size();
+    for (int i = 0; i < n; ++i) {
+      m->h_map[i] = rows[i];
+      m->h_map[n + i] = orig[rows[i]];
+    }
+    HIP_TRY(hipMemcpyAsync(m->d_map, m->h_map, 2 * n * sizeof(int32_t), hipMemcpyHostToDevice, s));
+    HIP_TRY(launch_scatter_rows(cur.tokens, cur.passes, m->d_map, m->d_map + n, n, L, n_blocks,
+                                d_out_tokens, m->s_final_passes, s));
+    return CORA_OK;
+  };
   for (;;) {
     if (cora_status e = denoise_step(m, &st, sc, gt, s)) return e;
     ++total;
-    HIP_TRY(hipMemcpyAsync(m->h_block, st.block_idx, B * sizeof(int32_t), hipMemcpyDeviceToHost,
+    HIP_TRY(hipMemcpyAsync(m->h_block, st.block_idx, Bc * sizeof(int32_t), hipMemcpyDeviceToHost,
                            s));
-    HIP_TRY(hipStreamSynchronize(s));
-    bool all = true;
-    for (int b = 0; b < B; ++b) all = all && m->h_block[b] >= n_blocks;
-    if (all) break;
+    HIP_TRY(hipStreamSynchronize(s));  // also: every earlier use of h_map has completed
+    std::vector<int32_t> fin, live;
+    for (int b = 0; b < Bc; ++b) (m->h_block[b] >= n_blocks ? fin : live).push_back(b);
+    if (live.empty()) break;
     if (total > max_passes)
       return fail(CORA_ERR_STATE, "decode did not terminate within the dense horizon");
+    if (!m->compaction || fin.empty()) continue;
+    if (cora_status e = write_out(fin)) return e;
+    const int nl = (int)live.size();
+    for (int i = 0; i < nl; ++i) m->h_map[2 * fin.size() + i] = live[i];
+    HIP_TRY(hipMemcpyAsync(m->d_map + 2 * fin.size(), m->h_map + 2 * fin.size(),
+                           nl * sizeof(int32_t), hipMemcpyHostToDevice, s));
+    HIP_TRY(launch_gather_state(cur, alt, m->d_map + 2 * fin.size(), nl, L, n_blocks, s));
+    std::swap(cur, alt);
+    std::vector<int32_t> o(nl);
+    for (int i = 0; i < nl; ++i) o[i] = orig[live[i]];
+    orig.swap(o);
+    Bc = nl;
+    st.tokens = cur.tokens; st.unresolved = cur.unresolved; st.prev_top1 = cur.prev;
+    st.persist = cur.persist; st.block_idx = cur.block_idx; st.step_idx = cur.step_idx;
+    st.passes = cur.passes; st.B = Bc;
   }
-  HIP_TRY(hipMemcpyAsync(d_out_tokens, st.tokens, (size_t)B * L * sizeof(int32_t),
-                         hipMemcpyDeviceToDevice, s));
-  HIP_TRY(hipMemcpyAsync(h_passes, st.passes, (size_t)B * n_blocks * sizeof(int32_t),
+  std::vector<int32_t> rest(Bc);
+  for (int b = 0; b < Bc; ++b) rest[b] = b;
+  if (cora_status e = write_out(rest)) return e;
+  HIP_TRY(hipMemcpyAsync(h_passes, m->s_final_passes, (size_t)B * n_blocks * sizeof(int32_t),
                          hipMemcpyDeviceToHost, s));
   HIP_TRY(hipStreamSynchronize(s));
   if (h_total_passes) *h_total_passes = (int32_t)total;

@@ -376,3 +376,35 @@ def test_eos_aware_block_decode(scope):
     cut = int(np.nonzero(gen == eos)[0][0])
     assert (passes[0, cut // BLK + 1:] == 0).all()
     assert (gen != spec.mask_id).all() and (y[1, P:] != spec.mask_id).all()
+
+
+@pytest.mark.parametrize("scope", [0, 1])
+def test_compacted_block_decode(scope):
+    """Batch-row compaction: rows cut by the EOS-aware controller finish at different
+    passes and leave the dense pass.  On this model no kernel's split of the work depends
+    on the row count, so the compacted decode must equal the uncompacted one bit for bit,
+    and every row must equal a decode of that row alone."""
+    require_gpu()
+    from paper_2608_11235_amd import Gate, Model, Sched
+    spec = SEPARATED
+    B = 3
+    prompt = si.prompt_tokens(4, B, P, spec.vocab, spec.mask_id)
+    gate = Gate(0.3, 1, True, scope)
+    with Model(spec, seed=0, max_batch=B, max_seq=L) as m:
+        y0, _, _ = m.block_decode(to_dev(prompt), G, Sched(BLK, S), gate)
+        eos = int(y0.cpu().numpy()[0, P + 5])
+        sched = Sched(BLK, S, eos)
+        out_c, passes_c, total_c = m.block_decode(to_dev(prompt), G, sched, gate)
+        m.set_compaction(False)
+        out_u, passes_u, total_u = m.block_decode(to_dev(prompt), G, sched, gate)
+        m.set_compaction(True)
+        alone = [m.block_decode(to_dev(prompt[b:b + 1]), G, sched, gate) for b in range(B)]
+    yc, yu = out_c.cpu().numpy(), out_u.cpu().numpy()
+    log_case(f"compaction scope={scope}: passes per row {passes_c.sum(1).tolist()}, "
+             f"total {total_c}")
+    assert (yc == yu).all() and (passes_c == passes_u).all() and total_c == total_u
+    rows = passes_c.sum(1)
+    assert rows.min() < rows.max(), "rows should finish at different passes"
+    for b in range(B):
+        assert (alone[b][0].cpu().numpy()[0] == yc[b]).all(), f"row {b} alone"
+        assert (alone[b][1][0] == passes_c[b]).all(), f"row {b} passes"
