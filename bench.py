@@ -31,18 +31,31 @@ DELTA_P, M_REQ = 0.65, 1
 
 # HBM bytes per launch from rocprofv3 FETCH_SIZE (x2.0) + WRITE_SIZE (x1.0) runs, scaled by a
 # plain 1 GiB copy (profiles/gate_up_gemm_llada8b_gen256.md, profiles/vocab_gate_8x512x126464.md).
-# Valid only for the kernel source the counters were taken on.
+# Valid only for the kernel source the counters were taken on: the digest covers the kernel's
+# file and the shared device headers.
+SHARED_SOURCES = ("paper_2608_11235_amd/csrc/common.hpp", "paper_2608_11235_amd/csrc/internal.hpp")
 COUNTER_TRAFFIC = {
-    "gate_up": ("paper_2608_11235_amd/csrc/gemm.hip", "6dd886b32a1882aa", 247652984),
-    "vocab_gate": ("paper_2608_11235_amd/csrc/vocab_gate.hip", "7d2ce1844c851bce", 1036512864),
+    "gate_up": ("paper_2608_11235_amd/csrc/gemm.hip", "f0b59267380e9fa7", 247614059),
+    "vocab_gate": ("paper_2608_11235_amd/csrc/vocab_gate.hip", "811bb73db6a53c1f", 1036531363),
 }
+
+
+def source_digest(path):
+    h = hashlib.sha256()
+    for p in (path,) + SHARED_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def note(msg):
+    """Progress line on stderr (stdout carries the one JSON result line)."""
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
 def counter_traffic(name):
     path, digest, nbytes = COUNTER_TRAFFIC[name]
-    with open(os.path.join(ROOT, path), "rb") as f:
-        now = hashlib.sha256(f.read()).hexdigest()[:16]
-    return nbytes if now == digest else None
+    return nbytes if digest is not None and source_digest(path) == digest else None
 
 
 def pass_flops(spec, M, rows):
@@ -353,6 +366,7 @@ def main():
     t1 = time.perf_counter()
     gu_ms, gu_launches = model.read_timing()
     model.set_timing(False)
+    note(f"timed passes done: {args.steps} in {t1 - t0:.3f} s")
     elapsed = t1 - t0
     committed = unres0 - int(st.unresolved.sum())
     passes_per_s = args.steps / elapsed
@@ -405,13 +419,19 @@ def main():
     del model
     torch.cuda.empty_cache()
 
+    if not args.no_decode:
+        note("block decode leg done")
     if not args.no_vocab:
         result["vocab_gate_roofline"] = vocab_gate_roofline()
+        note("vocab/gate leg done")
     if not args.no_gated:
         result["gated_decode_logits_x8"] = gated_decode_leg()
+        note("gated decode leg done")
     if not args.no_compaction:
         result["compaction_b8_logits_x8"] = compaction_leg()
+        note("compaction leg done")
     if not args.no_cpu_baseline:
+        note("cpu baseline leg starts")
         import seeded_inputs as si_
         try:
             result["cpu_baseline"] = cpu_baseline(si_.LLADA_8B, prompt)
