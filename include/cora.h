@@ -211,10 +211,13 @@ cora_status cora_block_decode(cora_model *model, const int32_t *d_prompt, int32_
  * `bytes` must equal the tensor's size.  Synchronous. */
 cora_status cora_model_copy_tensor(cora_model *model, int32_t tensor_id, void *h_dst, size_t bytes);
 
-/* Kernel timing: when enabled, the library brackets every launch of the
- * gate/up SwiGLU GEMM with HIP events on the launching stream.  Reading
- * returns the summed event time (ms) and the number of launches since the
- * last reset, waiting for the recorded events. */
+/* Kernel timing: while enabled, every launch of the gate/up SwiGLU GEMM is
+ * dispatched with a pair of HIP events (hipExtLaunchKernel) that the dispatch
+ * stamps with the kernel's start and end on the launching stream.  Enabling
+ * and disabling keep what was recorded, so timing can cover a sample of the
+ * launches.  Reading waits for the recorded events, returns the summed event
+ * time (ms) and the number of timed launches since the previous read, and
+ * clears both. */
 cora_status cora_model_set_timing(cora_model *model, int32_t enable);
 /* Batch-row compaction in cora_block_decode (R15: rows decode independently, so
  * dropping finished rows from the dense pass changes no live row's inputs; row

@@ -38,6 +38,8 @@
 //                         transposed v written straight from the accumulators.
 // Requirements: K % (64 * splits) == 0; M, N arbitrary (tails clamped on load, masked
 // on store).
+#include <hip/hip_ext.h>
+
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -463,26 +465,34 @@ GemmPlan gemm_plan_split(int M, int N, int K, int num_cus) {
   return best;
 }
 
+// With timing events, the dispatch itself stamps them with the kernel's start and end
+// (hipExtLaunchKernel), so no marker packet sits between the events and the kernel.
 template <int WAVES_M, int WAVES_N, int TM, int TN, int EPI, int PIPE>
-static hipError_t run(const GemmArgs& a, int grid, hipStream_t s) {
-  hipLaunchKernelGGL((k_gemm<WAVES_M, WAVES_N, TM, TN, EPI, PIPE>), dim3(grid),
-                     dim3(WAVES_M * WAVES_N * 64), 0, s, a);
+static hipError_t run(const GemmArgs& a, int grid, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  if (e0 || e1)
+    hipExtLaunchKernelGGL((k_gemm<WAVES_M, WAVES_N, TM, TN, EPI, PIPE>), dim3(grid),
+                          dim3(WAVES_M * WAVES_N * 64), 0, s, e0, e1, 0, a);
+  else
+    hipLaunchKernelGGL((k_gemm<WAVES_M, WAVES_N, TM, TN, EPI, PIPE>), dim3(grid),
+                       dim3(WAVES_M * WAVES_N * 64), 0, s, a);
   return hipGetLastError();
 }
 
 template <int EPI>
-static hipError_t run_cfg(int cfg, const GemmArgs& a, int grid, hipStream_t s) {
+static hipError_t run_cfg(int cfg, const GemmArgs& a, int grid, hipStream_t s, hipEvent_t e0,
+                          hipEvent_t e1) {
   switch (cfg) {
-    case 0: return run<4, 4, 2, 2, EPI, 0>(a, grid, s);
+    case 0: return run<4, 4, 2, 2, EPI, 0>(a, grid, s, e0, e1);
     case 1:
-      if constexpr (EPI == EPI_SWIGLU) return run<1, 2, 1, 2, EPI, 1>(a, grid, s);
-      else return run<1, 4, 1, 1, EPI, 1>(a, grid, s);
-    case 3: return run<4, 3, 2, 2, EPI, 2>(a, grid, s);
-    default: return run<4, 2, 2, 2, EPI, 2>(a, grid, s);
+      if constexpr (EPI == EPI_SWIGLU) return run<1, 2, 1, 2, EPI, 1>(a, grid, s, e0, e1);
+      else return run<1, 4, 1, 1, EPI, 1>(a, grid, s, e0, e1);
+    case 3: return run<4, 3, 2, 2, EPI, 2>(a, grid, s, e0, e1);
+    default: return run<4, 2, 2, 2, EPI, 2>(a, grid, s, e0, e1);
   }
 }
 
-hipError_t launch_gemm(int epi, const GemmArgs& in, const GemmPlan& p, hipStream_t s) {
+hipError_t launch_gemm(int epi, const GemmArgs& in, const GemmPlan& p, hipStream_t s,
+                       hipEvent_t ev_start, hipEvent_t ev_stop) {
   if (in.M == 0 || in.N == 0) return hipSuccess;
   if (p.splits < 1 || in.K % (BK * p.splits) != 0) return hipErrorInvalidValue;
   if (p.splits > 1 && epi != EPI_PART_F32) return hipErrorInvalidValue;
@@ -490,11 +500,11 @@ hipError_t launch_gemm(int epi, const GemmArgs& in, const GemmPlan& p, hipStream
   a.splits = p.splits;
   const int grid = p.tiles * p.splits;
   switch (epi) {
-    case EPI_BF16: return run_cfg<EPI_BF16>(p.cfg, a, grid, s);
-    case EPI_ADD_F32: return run_cfg<EPI_ADD_F32>(p.cfg, a, grid, s);
-    case EPI_SWIGLU: return run_cfg<EPI_SWIGLU>(p.cfg, a, grid, s);
-    case EPI_QKV_ROPE: return run_cfg<EPI_QKV_ROPE>(p.cfg, a, grid, s);
-    case EPI_PART_F32: return run_cfg<EPI_PART_F32>(p.cfg, a, grid, s);
+    case EPI_BF16: return run_cfg<EPI_BF16>(p.cfg, a, grid, s, ev_start, ev_stop);
+    case EPI_ADD_F32: return run_cfg<EPI_ADD_F32>(p.cfg, a, grid, s, ev_start, ev_stop);
+    case EPI_SWIGLU: return run_cfg<EPI_SWIGLU>(p.cfg, a, grid, s, ev_start, ev_stop);
+    case EPI_QKV_ROPE: return run_cfg<EPI_QKV_ROPE>(p.cfg, a, grid, s, ev_start, ev_stop);
+    case EPI_PART_F32: return run_cfg<EPI_PART_F32>(p.cfg, a, grid, s, ev_start, ev_stop);
   }
   return hipErrorInvalidValue;
 }

@@ -89,7 +89,9 @@ GemmPlan gemm_plan_split(int M, int N, int K, int num_cus);
 GemmPlan gemm_plan_cfg(int M, int N, int K, int cfg, int splits);
 int gemm_num_cfgs();
 inline size_t gemm_ws_floats_bound(int num_cus) { return (size_t)2 * num_cus * 256 * 256; }
-hipError_t launch_gemm(int epi, const GemmArgs& a, const GemmPlan& p, hipStream_t s);
+// ev_start / ev_stop (optional): stamped with the kernel's start and end by the dispatch
+hipError_t launch_gemm(int epi, const GemmArgs& a, const GemmPlan& p, hipStream_t s,
+                       hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr);
 // EPI_PART_F32 partials [splits][M][N] of the QKV projection -> the EPI_QKV_ROPE outputs.
 hipError_t launch_qkv_finish(const float* part, int splits, int M, int N, const float* bias,
                              const QkvOut& o, hipStream_t s);

@@ -317,8 +317,8 @@ extern "C" cora_status cora_model_device_bytes(cora_model* m, size_t* wbytes, si
 }
 
 // ---- timing ------------------------------------------------------------------------------
-// Timing events record without a system-scope fence: a measurement event must not add an
-// L2 writeback / invalidate around the kernel it brackets.
+// Timing events are created without a system-scope fence and handed to the kernel launch,
+// which stamps them with the kernel's own start and end.
 static cora_status grow_events(cora_model* m, size_t n) {
   while (m->ev.size() < n) {
     hipEvent_t e;
@@ -334,12 +334,10 @@ extern "C" cora_status cora_model_set_compaction(cora_model* m, int32_t enable) 
   return CORA_OK;
 }
 
+// Turning timing on or off keeps what has been recorded; read_timing returns and clears it.
 extern "C" cora_status cora_model_set_timing(cora_model* m, int32_t enable) {
   if (!m) return fail(CORA_ERR_INVALID_ARG, "null model");
   m->timing = enable != 0;
-  m->ev_used = 0;
-  m->acc_ms = 0.0;
-  m->launches = 0;
   // created up front so the timed passes do not pay for them
   if (m->timing)
     if (cora_status st = grow_events(m, 2 * m->layers.size() * 64)) return st;
@@ -363,24 +361,32 @@ extern "C" cora_status cora_model_read_timing(cora_model* m, double* total_ms, i
   if (cora_status st = drain_events(m)) return st;
   if (total_ms) *total_ms = m->acc_ms;
   if (launches) *launches = m->launches;
+  m->acc_ms = 0.0;
+  m->launches = 0;
   return CORA_OK;
 }
 
-static cora_status timed_event(cora_model* m, hipStream_t s) {
-  if (m->ev_used == m->ev.size()) {
+// the next free (start, stop) event pair
+static cora_status timed_pair(cora_model* m, hipEvent_t* e0, hipEvent_t* e1) {
+  if (m->ev_used + 2 > m->ev.size()) {
     if (m->ev.size() >= 8192) {
       if (cora_status st = drain_events(m)) return st;
     } else {
       if (cora_status st = grow_events(m, m->ev.size() + 64)) return st;
     }
   }
-  HIP_TRY(hipEventRecord(m->ev[m->ev_used++], s));
+  *e0 = m->ev[m->ev_used++];
+  *e1 = m->ev[m->ev_used++];
   return CORA_OK;
 }
 
 // ---- one dense pass ----------------------------------------------------------------------
-static cora_status gemm(cora_model* m, int epi, const GemmArgs& g, hipStream_t s) {
-  HIP_TRY(launch_gemm(epi, g, gemm_plan(g.M, g.N, g.K, m->num_cus), s));
+static cora_status gemm(cora_model* m, int epi, const GemmArgs& g, hipStream_t s,
+                        bool timed = false) {
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (timed)
+    if (cora_status st = timed_pair(m, &e0, &e1)) return st;
+  HIP_TRY(launch_gemm(epi, g, gemm_plan(g.M, g.N, g.K, m->num_cus), s, e0, e1));
   return CORA_OK;
 }
 
@@ -444,11 +450,7 @@ static cora_status run_layers(cora_model* m, const int32_t* tokens, int B, int L
     g = GemmArgs{m->attn, m->hq, ly.wo, m->hq, M, d, m->hq, m->h, d, nullptr, 1.0f};
     if (cora_status st = residual_gemm(m, g, m->a, s)) return st;
     g = GemmArgs{m->a, d, ly.wgu, d, M, 2 * m->f_pad, d, m->u, m->f_pad, nullptr, 1.0f};
-    if (m->timing)
-      if (cora_status st = timed_event(m, s)) return st;
-    if (cora_status st = gemm(m, EPI_SWIGLU, g, s)) return st;
-    if (m->timing)
-      if (cora_status st = timed_event(m, s)) return st;
+    if (cora_status st = gemm(m, EPI_SWIGLU, g, s, m->timing)) return st;
     g = GemmArgs{m->u, m->f_pad, ly.wd, m->f_pad, M, d, m->f_pad, m->h, d, nullptr, 1.0f};
     // the last layer's output is normalised only on the rows the LM head reads
     if (cora_status st = residual_gemm(m, g, l + 1 < n_layers ? m->a : nullptr, s)) return st;
