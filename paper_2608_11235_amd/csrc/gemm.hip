@@ -63,6 +63,17 @@ __device__ __forceinline__ void buf_load_tail(u32x4_t (&r)[N], __amdgpu_buffer_r
         u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, i + 1 < N ? voff : voff_last, i * step, 0));
 }
 
+// n 16-byte loads at per-chunk byte offsets voff[i] + koff (koff uniform); when the chunks
+// do not divide evenly and EXACT is false, the last one only where last_ok
+template <int N, bool EXACT>
+__device__ __forceinline__ void buf_load_chunks(u32x4_t (&r)[N], __amdgpu_buffer_rsrc_t rs,
+                                                const int (&voff)[N], int koff, bool last_ok) {
+#pragma unroll
+  for (int i = 0; i < N; ++i)
+    if (EXACT || i + 1 < N || last_ok)
+      r[i] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, voff[i] + koff, 0, 0));
+}
+
 template <int N, bool EXACT>
 __device__ __forceinline__ void buf_load(u32x4_t (&r)[N], __amdgpu_buffer_rsrc_t rs, int voff,
                                          int step, bool last_ok) {
@@ -111,13 +122,32 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void k_gemm(GemmArgs g) {
       0x00020000);
   const int c_r = tid >> 3, c_k = (tid & 7) * 8;
   const int a_off = (int)(((int64_t)(m0 + c_r) * g.lda + k_base + c_k) * 2);
-  const int b_off = (int)(((int64_t)(n0 + c_r) * g.ldw + k_base + c_k) * 2);
+  const int b_off = (int)(((int64_t)(n0 + c_r) * g.ldw + k_base + c_k) * 2);  // row-major
   const int a_step = (NT / 8) * (int)g.lda * 2;  // next chunk of this thread: NT/8 rows down
   const int b_step = (NT / 8) * (int)g.ldw * 2;
   const int lds_off = c_r * LDK + c_k;
   constexpr int LDS_STEP = (NT / 8) * LDK;
   const bool a_last = tid + (CA - 1) * NT < BM * BK / 8;
   const bool b_last = tid + (CB - 1) * NT < BN * BK / 8;
+  // B chunk i of slice kt sits at byte b_chunk[i] + kt * b_kstride: row-major weights (row
+  // c_r + i NT / 8 of the tile, next slice 128 bytes on) or weights packed in 64 x 64 blocks
+  // (row-major inside, block (row / 64, k / 64) at (row / 64 * K / 64 + k / 64) * 8 KB, next
+  // slice 8 KB on: a tile slice reads whole 8 KB blocks).  A chunk past the tile or past N
+  // reads from the first byte past the operand: zeros, no memory traffic.
+  const int b_oob = (int)(b_bytes > 0x7fffffffLL ? 0x7fffffff : b_bytes);
+  const int b_kstride = g.w_packed ? 64 * BK * 2 : BK * 2;
+  int b_chunk[CB];
+#pragma unroll
+  for (int i = 0; i < CB; ++i) {
+    const int j = tid + i * NT, row = j >> 3;
+    const bool in = j < BN * BK / 8 && n0 + row < g.N;
+    if (!g.w_packed)
+      b_chunk[i] = in ? b_off + i * b_step : b_oob;
+    else
+      b_chunk[i] = in ? (int)((((int64_t)((n0 + row) >> 6) * (g.K / 64) + k_base / 64) * 4096 +
+                               (row & 63) * 64 + (j & 7) * 8) * 2)
+                      : b_oob;
+  }
 
   f32x16_t acc[TM][TN];
 #pragma unroll
@@ -132,7 +162,7 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void k_gemm(GemmArgs g) {
 #define GEMM_FETCH(ra, rb, kt)                                            \
   do {                                                                    \
     buf_load<CA, A_EXACT>(ra, a_rs, a_off + (kt) * BK * 2, a_step, a_last); \
-    buf_load<CB, B_EXACT>(rb, b_rs, b_off + (kt) * BK * 2, b_step, b_last); \
+    buf_load_chunks<CB, B_EXACT>(rb, b_rs, b_chunk, (kt) * b_kstride, b_last); \
   } while (0)
   auto stash = [&](int buf, const u32x4_t(&ra)[CA], const u32x4_t(&rb)[CB]) {
 #pragma unroll
@@ -198,11 +228,10 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void k_gemm(GemmArgs g) {
     // a thread's chunk past the tile (CA * NT / 8 > BM) reads from the first byte past the
     // operand: zeros, no memory traffic
     const int a_tail = A_EXACT || a_last ? a_off : (int)(a_bytes > 0x7fffffffLL ? 0x7fffffff : a_bytes);
-    const int b_tail = B_EXACT || b_last ? b_off : (int)(b_bytes > 0x7fffffffLL ? 0x7fffffff : b_bytes);
 #define FETCH_ALL(ra, rb, kt)                                                              \
   do {                                                                                     \
     buf_load_tail<CA>(ra, a_rs, a_off + (kt) * BK * 2, a_tail + (kt) * BK * 2, a_step);    \
-    buf_load_tail<CB>(rb, b_rs, b_off + (kt) * BK * 2, b_tail + (kt) * BK * 2, b_step);    \
+    buf_load_chunks<CB, true>(rb, b_rs, b_chunk, (kt) * b_kstride, true);                 \
   } while (0)
 #define SG(mask, n) __builtin_amdgcn_sched_group_barrier(mask, n, 0)
     // slice KT out of LDS buffer KT & 1; RAN/RBN hold slice KT+1 on entry and receive

@@ -13,7 +13,7 @@ namespace cora {
 enum RowMap { ROW_IDENTITY = 0, ROW_GATE = 1, ROW_UP = 2, ROW_ROPE_PAIR = 3 };
 hipError_t launch_init_bf16(uint16_t* dst, uint64_t seed, uint64_t tensor_id, int64_t rows,
                             int64_t cols, int64_t ld, int row_map, int64_t row_offset, double std_dev,
-                            int head_dim, hipStream_t s);
+                            int head_dim, hipStream_t s, bool packed = false);
 hipError_t launch_init_f32(float* dst, uint64_t seed, uint64_t tensor_id, int64_t n, double std_dev,
                            int pair_head_dim, hipStream_t s);
 // physical position of logical index j inside a head of hd pair-interleaved rows
@@ -77,6 +77,7 @@ struct GemmArgs {
   float scale;         // EPI_BF16: multiplier after the bias
   int splits;          // set by launch_gemm from the plan
   QkvOut qkv;          // EPI_QKV_ROPE destinations
+  bool w_packed;       // W in 64 x 64 blocks (N % 64 == 0, K % 64 == 0), see pack layout
 };
 struct GemmPlan {
   int cfg, tiles, splits;

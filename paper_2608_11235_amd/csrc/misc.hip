@@ -26,19 +26,26 @@ __device__ __forceinline__ float normal_from_counter(uint64_t key, uint64_t ctr,
   return (float)(std_dev * n);
 }
 
+// element (pr, c) of the physical matrix goes to pr * ld + c, or, packed (ld % 64 == 0), to
+// block (pr / 64, c / 64) of 64 x 64 (row-major inside), blocks ordered by row block then
+// column block
+__device__ __forceinline__ int64_t packed64_index(int64_t pr, int64_t c, int64_t ld) {
+  return ((pr >> 6) * (ld >> 6) + (c >> 6)) * 4096 + (pr & 63) * 64 + (c & 63);
+}
+
 __global__ void k_init_bf16(uint16_t* __restrict__ dst, uint64_t key, uint64_t base, int64_t rows,
                             int64_t cols, int64_t ld, int row_map, int64_t row_offset,
-                            double std_dev, int hd) {
+                            double std_dev, int hd, int packed) {
   for (int64_t r = blockIdx.x; r < rows; r += gridDim.x) {
     int64_t pr;
     if (row_map == ROW_GATE) pr = (r >> 5) * 64 + (r & 31);
     else if (row_map == ROW_UP) pr = (r >> 5) * 64 + 32 + (r & 31);
     else if (row_map == ROW_ROPE_PAIR) pr = row_offset + (r / hd) * hd + rope_pair_pos((int)(r % hd), hd);
     else pr = row_offset + r;
-    uint16_t* out = dst + pr * ld;
     for (int64_t c = threadIdx.x; c < cols; c += blockDim.x) {
       const uint64_t ctr = base | (uint64_t)(r * cols + c);
-      out[c] = (uint16_t)f32_to_bf16_bits(normal_from_counter(key, ctr, std_dev));
+      dst[packed ? packed64_index(pr, c, ld) : pr * ld + c] =
+          (uint16_t)f32_to_bf16_bits(normal_from_counter(key, ctr, std_dev));
     }
   }
 }
@@ -71,10 +78,12 @@ static uint64_t host_mix64(uint64_t z) {
 
 hipError_t launch_init_bf16(uint16_t* dst, uint64_t seed, uint64_t tensor_id, int64_t rows,
                             int64_t cols, int64_t ld, int row_map, int64_t row_offset, double std_dev,
-                            int head_dim, hipStream_t s) {
+                            int head_dim, hipStream_t s, bool packed) {
+  if (packed && ld % 64 != 0) return hipErrorInvalidValue;
   const int grid = (int)(rows < 16384 ? rows : 16384);
   hipLaunchKernelGGL(k_init_bf16, dim3(grid), dim3(256), 0, s, dst, host_mix64(seed),
-                     tensor_id << 40, rows, cols, ld, row_map, row_offset, std_dev, head_dim);
+                     tensor_id << 40, rows, cols, ld, row_map, row_offset, std_dev, head_dim,
+                     packed ? 1 : 0);
   return hipGetLastError();
 }
 

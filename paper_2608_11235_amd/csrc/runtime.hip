@@ -4,6 +4,7 @@
 #include <string.h>
 
 #include <string>
+#include <algorithm>
 #include <vector>
 
 #include "common.hpp"
@@ -111,6 +112,14 @@ static cora_status validate_cfg(const cora_model_cfg& c) {
     return fail(CORA_ERR_UNSUPPORTED, "d_model and n_heads*head_dim must be multiples of 64");
   if (c.d_model > RESIDUAL_NORM_MAX_D)
     return fail(CORA_ERR_UNSUPPORTED, "d_model must not exceed 8192");
+  {
+    // the GEMMs address every layer matrix with 32-bit byte offsets
+    const int64_t hq = (int64_t)c.n_heads * c.head_dim, hkv = (int64_t)c.n_kv_heads * c.head_dim;
+    const int64_t fp = ((int64_t)c.ffn_dim + 63) / 64 * 64, d = c.d_model;
+    const int64_t largest = std::max({(hq + 2 * hkv) * d, d * hq, 2 * fp * d, d * fp});
+    if (largest * 2 + std::max({d, hq, fp}) * 128 > 0x7fffffffLL)
+      return fail(CORA_ERR_UNSUPPORTED, "a layer weight matrix exceeds 2 GB");
+  }
   if (!(c.rms_eps > 0.f) || !(c.rope_theta > 0.f) || !isfinite(c.logit_scale) ||
       !(c.init_std >= 0.0))
     return fail(CORA_ERR_INVALID_ARG, "rms_eps, rope_theta must be > 0; logit_scale finite");
@@ -271,16 +280,16 @@ extern "C" cora_status cora_model_create(const cora_model_cfg* cfg, uint64_t see
     for (int l = 0; l < (int)L_; ++l) {
       const auto& ly = m->layers[l];
       const uint64_t t0 = 100 + 16 * (uint64_t)l;
-      HIP_TRY(launch_init_bf16(ly.wqkv, seed, t0 + 0, m->hq, d, d, ROW_ROPE_PAIR, 0, sd, hd, s));
+      HIP_TRY(launch_init_bf16(ly.wqkv, seed, t0 + 0, m->hq, d, d, ROW_ROPE_PAIR, 0, sd, hd, s, true));
       HIP_TRY(launch_init_bf16(ly.wqkv, seed, t0 + 1, m->hkv, d, d, ROW_ROPE_PAIR, m->hq, sd, hd,
-                               s));
+                               s, true));
       HIP_TRY(launch_init_bf16(ly.wqkv, seed, t0 + 2, m->hkv, d, d, ROW_IDENTITY, m->hq + m->hkv,
-                               sd, hd, s));
-      HIP_TRY(launch_init_bf16(ly.wo, seed, t0 + 3, d, m->hq, m->hq, ROW_IDENTITY, 0, sd, hd, s));
-      HIP_TRY(launch_init_bf16(ly.wgu, seed, t0 + 4, cfg->ffn_dim, d, d, ROW_GATE, 0, sd, hd, s));
-      HIP_TRY(launch_init_bf16(ly.wgu, seed, t0 + 5, cfg->ffn_dim, d, d, ROW_UP, 0, sd, hd, s));
+                               sd, hd, s, true));
+      HIP_TRY(launch_init_bf16(ly.wo, seed, t0 + 3, d, m->hq, m->hq, ROW_IDENTITY, 0, sd, hd, s, true));
+      HIP_TRY(launch_init_bf16(ly.wgu, seed, t0 + 4, cfg->ffn_dim, d, d, ROW_GATE, 0, sd, hd, s, true));
+      HIP_TRY(launch_init_bf16(ly.wgu, seed, t0 + 5, cfg->ffn_dim, d, d, ROW_UP, 0, sd, hd, s, true));
       HIP_TRY(launch_init_bf16(ly.wd, seed, t0 + 6, d, cfg->ffn_dim, m->f_pad, ROW_IDENTITY, 0, sd,
-                               hd, s));
+                               hd, s, true));
       if (cfg->qkv_bias) {
         HIP_TRY(launch_init_f32(ly.bqkv, seed, t0 + 7, m->hq, sd, hd, s));
         HIP_TRY(launch_init_f32(ly.bqkv + m->hq, seed, t0 + 8, m->hkv, sd, hd, s));
@@ -442,16 +451,20 @@ static cora_status run_layers(cora_model* m, const int32_t* tokens, int B, int L
     const auto& ly = m->layers[l];
     // m->a holds rmsnorm(h) of this layer's input
     GemmArgs g{m->a, d, ly.wqkv, d, M, m->qkv_n, d, nullptr, 0, ly.bqkv, 1.0f};
+    g.w_packed = true;
     g.qkv = QkvOut{m->q, m->k, m->vt, m->rope_cos, m->rope_sin, L, Ls, c.n_heads, c.n_kv_heads,
                    c.head_dim};
     if (cora_status st = qkv_gemm(m, g, s)) return st;
     HIP_TRY(launch_attention(m->q, m->k, m->vt, m->attn, B, L, Ls, c.n_heads, c.n_kv_heads,
                              c.head_dim, m->num_cus, s));
     g = GemmArgs{m->attn, m->hq, ly.wo, m->hq, M, d, m->hq, m->h, d, nullptr, 1.0f};
+    g.w_packed = true;
     if (cora_status st = residual_gemm(m, g, m->a, s)) return st;
     g = GemmArgs{m->a, d, ly.wgu, d, M, 2 * m->f_pad, d, m->u, m->f_pad, nullptr, 1.0f};
+    g.w_packed = true;
     if (cora_status st = gemm(m, EPI_SWIGLU, g, s, m->timing)) return st;
     g = GemmArgs{m->u, m->f_pad, ly.wd, m->f_pad, M, d, m->f_pad, m->h, d, nullptr, 1.0f};
+    g.w_packed = true;
     // the last layer's output is normalised only on the rows the LM head reads
     if (cora_status st = residual_gemm(m, g, l + 1 < n_layers ? m->a : nullptr, s)) return st;
   }
@@ -727,6 +740,19 @@ extern "C" cora_status cora_block_decode(cora_model* m, const int32_t* d_prompt,
 }
 
 // ---- weight read-back in logical [out, in] layout ---------------------------------------
+// Row-major host copy of a layer matrix stored in 64 x 64 blocks (physical rows x ld).
+static cora_status read_packed(const uint16_t* d_packed, int64_t rows, int64_t ld,
+                               std::vector<uint16_t>& out) {
+  std::vector<uint16_t> p((size_t)(rows * ld));
+  HIP_TRY(hipMemcpy(p.data(), d_packed, p.size() * 2, hipMemcpyDeviceToHost));
+  out.resize(p.size());
+  for (int64_t r = 0; r < rows; ++r)
+    for (int64_t c = 0; c < ld; ++c)
+      out[(size_t)(r * ld + c)] = p[(size_t)(((r >> 6) * (ld >> 6) + (c >> 6)) * 4096 +
+                                             (r & 63) * 64 + (c & 63))];
+  return CORA_OK;
+}
+
 extern "C" cora_status cora_model_copy_tensor(cora_model* m, int32_t tensor_id, void* h_dst,
                                               size_t bytes) {
   if (!m || !h_dst) return fail(CORA_ERR_INVALID_ARG, "null argument");
@@ -751,39 +777,42 @@ extern "C" cora_status cora_model_copy_tensor(cora_model* m, int32_t tensor_id, 
       const int rows = j == 0 ? m->hq : m->hkv;
       const int off = j == 0 ? 0 : (j == 1 ? m->hq : m->hq + m->hkv);
       if (cora_status e = want((size_t)rows * d)) return e;
-      if (j == 2) {
-        HIP_TRY(hipMemcpy(h_dst, ly.wqkv + (size_t)off * d, bytes, hipMemcpyDeviceToHost));
-        return CORA_OK;
-      }
-      std::vector<uint16_t> tmp((size_t)rows * d);  // undo the per-head pair interleave
-      HIP_TRY(hipMemcpy(tmp.data(), ly.wqkv + (size_t)off * d, bytes, hipMemcpyDeviceToHost));
+      std::vector<uint16_t> tmp;
+      if (cora_status e = read_packed(ly.wqkv, m->qkv_n, d, tmp)) return e;
       const int hd = c.head_dim;
-      for (int r = 0; r < rows; ++r) {
-        const size_t pr = (size_t)(r / hd) * hd + rope_pair_pos(r % hd, hd);
+      for (int r = 0; r < rows; ++r) {  // undo the per-head pair interleave of q and k
+        const size_t pr = off + (j == 2 ? r : (size_t)(r / hd) * hd + rope_pair_pos(r % hd, hd));
         memcpy(out + (size_t)r * d, tmp.data() + pr * d, (size_t)d * 2);
       }
       return CORA_OK;
     }
-    case 3:
+    case 3: {
       if (cora_status e = want((size_t)d * m->hq)) return e;
-      HIP_TRY(hipMemcpy(h_dst, ly.wo, bytes, hipMemcpyDeviceToHost));
+      std::vector<uint16_t> tmp;
+      if (cora_status e = read_packed(ly.wo, d, m->hq, tmp)) return e;
+      memcpy(out, tmp.data(), bytes);
       return CORA_OK;
+    }
     case 4: case 5: {
       const int F = c.ffn_dim;
       if (cora_status e = want((size_t)F * d)) return e;
-      std::vector<uint16_t> tmp((size_t)2 * m->f_pad * d);
-      HIP_TRY(hipMemcpy(tmp.data(), ly.wgu, tmp.size() * 2, hipMemcpyDeviceToHost));
+      std::vector<uint16_t> tmp;
+      if (cora_status e = read_packed(ly.wgu, 2 * (int64_t)m->f_pad, d, tmp)) return e;
       for (int r = 0; r < F; ++r) {
         const size_t pr = (size_t)(r >> 5) * 64 + (j == 5 ? 32 : 0) + (r & 31);
         memcpy(out + (size_t)r * d, tmp.data() + pr * d, (size_t)d * 2);
       }
       return CORA_OK;
     }
-    case 6:
+    case 6: {
       if (cora_status e = want((size_t)d * c.ffn_dim)) return e;
-      HIP_TRY(hipMemcpy2D(h_dst, (size_t)c.ffn_dim * 2, ly.wd, (size_t)m->f_pad * 2,
-                          (size_t)c.ffn_dim * 2, d, hipMemcpyDeviceToHost));
+      std::vector<uint16_t> tmp;
+      if (cora_status e = read_packed(ly.wd, d, m->f_pad, tmp)) return e;
+      for (int r = 0; r < d; ++r)
+        memcpy(out + (size_t)r * c.ffn_dim, tmp.data() + (size_t)r * m->f_pad,
+               (size_t)c.ffn_dim * 2);
       return CORA_OK;
+    }
     case 7: case 8: case 9: {
       if (!c.qkv_bias) return fail(CORA_ERR_INVALID_ARG, "model has no qkv bias");
       const int n = j == 7 ? m->hq : m->hkv;
