@@ -161,12 +161,15 @@ cora_status cora_forward_logits(cora_model *model, const int32_t *d_tokens, int3
  * vocab/gate kernels (Eq. 1, Eq. 2, transfer rule, Eq. 3, Eq. 4, termination;
  * see cora_vocab_gate).  top1/conf are [B, block_len] (the active block's
  * rows) under the BLOCK scope and [B, gen_len] (the generation region, LM head
- * and row reduction in chunks of up to 256 rows) under GLOBAL.  When a call
- * (or chunk) scores at most 64 rows in all, Eq. (1) is computed inside the
- * LM-head pass (per-128-entry partial max / first arg max / sum of exp,
- * merged in vocab order) and no logits are written; the top-1 is then the
- * same as cora_vocab_gate's on the logits cora_forward_logits writes for
- * those rows.  Asynchronous. */
+ * and row reduction in chunks of up to 256 rows) under GLOBAL.  Eq. (1) is
+ * computed inside the LM-head pass and no logits are written: a call (or
+ * chunk) that scores at most 64 rows in all streams the packed weight copy
+ * (per-128-entry partial max / first arg max / sum of exp), more rows reduce
+ * each wavefront's logit columns in the tiled GEMM's epilogue; the partials
+ * are merged in vocab order.  The top-1 is then the same as cora_vocab_gate's
+ * on the logits cora_forward_logits writes for those rows (same row count).
+ * Only a vocabulary too small for the partials to fit the logits buffer takes
+ * logits + row reduction.  Asynchronous. */
 cora_status cora_denoise_step(cora_model *model, cora_state *state, const cora_sched_cfg *sched,
                               const cora_gate_cfg *gate, void *hip_stream);
 

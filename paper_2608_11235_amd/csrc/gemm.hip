@@ -39,6 +39,7 @@
 // Requirements: K % (64 * splits) == 0; M, N arbitrary (tails clamped on load, masked
 // on store).
 #include <hip/hip_ext.h>
+#include <limits.h>
 
 #include "common.hpp"
 #include "internal.hpp"
@@ -387,6 +388,59 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void k_gemm(GemmArgs g) {
           }
         }
     }
+  } else if constexpr (EPI == EPI_TOP1) {
+    // Row statistics of Eq. (1) over this wavefront's TN x 32 columns.  Each 32 x 32 block
+    // passes through a per-wavefront LDS scratch as the rounded logits EPI_BF16 would write;
+    // lane l reduces row l % 32 over the block's columns 16 (l / 32) .. + 15, the two lanes
+    // of a row are merged (lower columns first), and the blocks of a block row are folded in
+    // column order.
+    constexpr int SP = 34;  // scratch row pitch, bf16
+    static_assert(sizeof(As) >= (size_t)WAVES_M * WAVES_N * 32 * SP * 2, "TOP1 scratch");
+    __syncthreads();  // every wavefront is done reading the operand tiles
+    uint16_t* scr = &As[0][0] + wave * 32 * SP;
+    const int rr = lane & 31, half = lane >> 5;
+    TopState rs[TM];
+#pragma unroll
+    for (int i = 0; i < TM; ++i) rs[i] = TopState{-INFINITY, 0.f, INT_MAX};
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e)
+          scr[(8 * (e >> 2) + row_q + (e & 3)) * SP + col_l] =
+              (uint16_t)f32_to_bf16_bits(acc[i][j][e] * g.scale);
+        __syncthreads();
+        const int c0 = n0 + wn * TN * 32 + j * 32 + half * 16;
+        float v[16];
+        TopState t{-INFINITY, 0.f, INT_MAX};
+#pragma unroll
+        for (int c = 0; c < 16; ++c) {
+          float x = bf16_bits_to_f32(scr[rr * SP + half * 16 + c]);
+          if (c0 + c >= g.N || c0 + c == g.mask_id) x = -INFINITY;
+          v[c] = x;
+          if (x > t.m) { t.m = x; t.arg = c0 + c; }
+        }
+        if (t.m != -INFINITY) {
+          const float ml = t.m * LOG2E;
+#pragma unroll
+          for (int c = 0; c < 16; ++c) t.s += fast_exp2(fmaf(v[c], LOG2E, -ml));
+        }
+        const TopState u{__shfl_xor(t.m, 32, 64), __shfl_xor(t.s, 32, 64), __shfl_xor(t.arg, 32, 64)};
+        rs[i] = merge(rs[i], half == 0 ? merge(t, u) : merge(u, t));
+        __syncthreads();  // the scratch is rewritten by the next block
+      }
+    const int part = tile_n * WAVES_N + wn;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      const int row = m0 + wm * TM * 32 + i * 32 + rr;
+      if (half == 0 && row < g.M) {
+        const int64_t o = (int64_t)row * g.n_parts + part;
+        g.part_m[o] = rs[i].m;
+        g.part_s[o] = rs[i].s;
+        g.part_arg[o] = rs[i].arg;
+      }
+    }
   } else {
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
@@ -434,6 +488,13 @@ static CfgShape cfg_shape(int cfg) {
 }
 
 int gemm_num_cfgs() { return 4; }
+
+// wavefront columns per tile and their width (TN x 32) of each config
+int gemm_top1_parts(const GemmPlan& p, int N) {
+  const CfgShape sh = cfg_shape(p.cfg);
+  const int waves_n = p.cfg == 0 ? 4 : (p.cfg == 1 ? 4 : (p.cfg == 3 ? 3 : 2));
+  return (N + sh.bn - 1) / sh.bn * waves_n;
+}
 
 // Relative main-loop efficiency of the large-tile configs (16, 12 and 8 waves per workgroup),
 // measured on the pass's shapes.
@@ -534,6 +595,10 @@ hipError_t launch_gemm(int epi, const GemmArgs& in, const GemmPlan& p, hipStream
     case EPI_SWIGLU: return run_cfg<EPI_SWIGLU>(p.cfg, a, grid, s, ev_start, ev_stop);
     case EPI_QKV_ROPE: return run_cfg<EPI_QKV_ROPE>(p.cfg, a, grid, s, ev_start, ev_stop);
     case EPI_PART_F32: return run_cfg<EPI_PART_F32>(p.cfg, a, grid, s, ev_start, ev_stop);
+    case EPI_TOP1:
+      if (a.n_parts != gemm_top1_parts(p, a.N) || !a.part_m || !a.part_s || !a.part_arg)
+        return hipErrorInvalidValue;
+      return run_cfg<EPI_TOP1>(p.cfg, a, grid, s, ev_start, ev_stop);
   }
   return hipErrorInvalidValue;
 }

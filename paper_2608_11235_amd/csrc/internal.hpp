@@ -55,7 +55,13 @@ hipError_t launch_scatter_rows(const int32_t* tokens, const int32_t* passes, con
                                int32_t* out_tokens, int32_t* out_passes, hipStream_t s);
 
 // ---- GEMM: C[M, N] = A[M, K] . W[N, K]^T, bf16 in, fp32 accumulate ---------------------
-enum GemmEpi { EPI_BF16 = 0, EPI_ADD_F32 = 1, EPI_SWIGLU = 2, EPI_QKV_ROPE = 3, EPI_PART_F32 = 4 };
+enum GemmEpi {
+  EPI_BF16 = 0, EPI_ADD_F32 = 1, EPI_SWIGLU = 2, EPI_QKV_ROPE = 3, EPI_PART_F32 = 4, EPI_TOP1 = 5
+};
+// EPI_TOP1: no C; per row and wavefront column range, the (max, lowest arg max, sum of
+// exp(l - max)) of the logits EPI_BF16 would write (bias none, then * scale, rounded to
+// bf16), mask_id and columns past N left out, at part_*[row * n_parts + p] with
+// p = column range index in vocab order (gemm_top1_parts ranges per row).
 // EPI_PART_F32: split s of the K loop stores its fp32 partial product to
 // ((float*)C)[s * M * ldc + row * ldc + col]; the partials are folded in by a later kernel
 // (launch_residual_norm), so the GEMM itself takes no tickets.
@@ -78,6 +84,9 @@ struct GemmArgs {
   int splits;          // set by launch_gemm from the plan
   QkvOut qkv;          // EPI_QKV_ROPE destinations
   bool w_packed;       // W in 64 x 64 blocks (N % 64 == 0, K % 64 == 0), see pack layout
+  // EPI_TOP1 outputs
+  float* part_m; float* part_s; int* part_arg;
+  int n_parts, mask_id;
 };
 struct GemmPlan {
   int cfg, tiles, splits;
@@ -93,6 +102,8 @@ inline size_t gemm_ws_floats_bound(int num_cus) { return (size_t)2 * num_cus * 2
 // ev_start / ev_stop (optional): stamped with the kernel's start and end by the dispatch
 hipError_t launch_gemm(int epi, const GemmArgs& a, const GemmPlan& p, hipStream_t s,
                        hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr);
+// EPI_TOP1 partials per row of a plan (column ranges of TN x 32 over the N tiles)
+int gemm_top1_parts(const GemmPlan& p, int N);
 // EPI_PART_F32 partials [splits][M][N] of the QKV projection -> the EPI_QKV_ROPE outputs.
 hipError_t launch_qkv_finish(const float* part, int splits, int M, int N, const float* bias,
                              const QkvOut& o, hipStream_t s);
@@ -120,6 +131,10 @@ hipError_t launch_lm_head(const LmHeadArgs& a, bool top1, hipStream_t s);
 // top1/conf[b * out_ld + out_off + r]
 hipError_t launch_top1_merge(const LmHeadArgs& a, int n_rows, int out_ld, int out_off,
                              int32_t* top1, float* conf, hipStream_t s);
+// the same merge for M rows of n_parts partials each (EPI_TOP1 GEMM output)
+hipError_t launch_top1_merge_parts(const float* pm, const float* ps, const int* pa, int n_parts,
+                                   int M, int n_rows, int out_ld, int out_off, int32_t* top1,
+                                   float* conf, hipStream_t s);
 
 // ---- attention ---------------------------------------------------------------------------
 hipError_t launch_attention(const uint16_t* q, const uint16_t* k, const uint16_t* vt,

@@ -311,12 +311,20 @@ hipError_t launch_lm_head(const LmHeadArgs& in, bool top1, hipStream_t s) {
   return hipGetLastError();
 }
 
+hipError_t launch_top1_merge_parts(const float* pm, const float* ps, const int* pa, int n_parts,
+                                   int M, int n_rows, int out_ld, int out_off, int32_t* top1,
+                                   float* conf, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  if (n_parts <= 0 || n_rows <= 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_top1_merge, dim3(M), dim3(256), 0, s, pm, ps, pa, n_parts, n_rows, out_ld,
+                     out_off, top1, conf);
+  return hipGetLastError();
+}
+
 hipError_t launch_top1_merge(const LmHeadArgs& a, int n_rows, int out_ld, int out_off,
                              int32_t* top1, float* conf, hipStream_t s) {
-  if (a.M <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_top1_merge, dim3(a.M), dim3(256), 0, s, a.part_m, a.part_s, a.part_arg,
-                     lm_head_parts(a.N), n_rows, out_ld, out_off, top1, conf);
-  return hipGetLastError();
+  return launch_top1_merge_parts(a.part_m, a.part_s, a.part_arg, lm_head_parts(a.N), a.M, n_rows,
+                                 out_ld, out_off, top1, conf, s);
 }
 
 }  // namespace cora

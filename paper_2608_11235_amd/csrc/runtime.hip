@@ -503,8 +503,10 @@ static cora_status lm_head(cora_model* m, const RowSel& sel, int n_out_rows, uin
   return gemm(m, EPI_BF16, g, s);
 }
 
-// Scores of the selected rows (Eq. 1) into top1/conf[b * out_ld + out_off + r]: fused into
-// the LM-head pass for few rows (no logits written), else logits then the row reduction.
+// Scores of the selected rows (Eq. 1) into top1/conf[b * out_ld + out_off + r], fused into
+// the LM-head pass (no logits written): the packed-weight stream for few rows, the tiled
+// GEMM's EPI_TOP1 epilogue for more; logits then the row reduction only where the partials
+// do not fit the logits buffer.
 static cora_status score_rows(cora_model* m, const RowSel& sel, int B, int n_rows,
                               const VocabGateArgs& vg, hipStream_t s) {
   const auto& c = m->cfg;
@@ -514,6 +516,26 @@ static cora_status score_rows(cora_model* m, const RowSel& sel, int B, int n_row
     const LmHeadArgs a = lm_args(m, M);
     HIP_TRY(launch_lm_head(a, true, s));
     HIP_TRY(launch_top1_merge(a, n_rows, vg.out_ld, vg.out_off, vg.top1, vg.conf, s));
+    return CORA_OK;
+  }
+  // more rows: the tiled GEMM folds each wavefront's logit columns into per-row partials
+  // (EPI_TOP1), held in the logits buffer, which this path leaves otherwise unused
+  const GemmPlan p = gemm_plan(M, c.vocab, c.d_model, m->num_cus);
+  const int np = gemm_top1_parts(p, c.vocab);
+  const size_t part_bytes = align_up((size_t)M * np * 4);
+  if (3 * part_bytes <= (size_t)m->max_batch * m->max_rows * c.vocab * 2) {
+    HIP_TRY(launch_rmsnorm(m->h, m->ones, m->a, M, c.d_model, c.rms_eps, sel, s));
+    GemmArgs g{m->a, c.d_model, m->lm_head, c.d_model, M, c.vocab, c.d_model, nullptr, 0,
+               nullptr, c.logit_scale};
+    char* buf = reinterpret_cast<char*>(m->logits);
+    g.part_m = reinterpret_cast<float*>(buf);
+    g.part_s = reinterpret_cast<float*>(buf + part_bytes);
+    g.part_arg = reinterpret_cast<int*>(buf + 2 * part_bytes);
+    g.n_parts = np;
+    g.mask_id = c.mask_id;
+    HIP_TRY(launch_gemm(EPI_TOP1, g, p, s));
+    HIP_TRY(launch_top1_merge_parts(g.part_m, g.part_s, g.part_arg, np, M, n_rows, vg.out_ld,
+                                    vg.out_off, vg.top1, vg.conf, s));
     return CORA_OK;
   }
   if (cora_status e = lm_head(m, sel, M, m->logits, s)) return e;
