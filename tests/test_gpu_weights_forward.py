@@ -93,11 +93,13 @@ def test_split_k_forward(B, L, row_begin, n_rows):
     _check_logits(MID_SPLIT, B, L, row_begin, n_rows)
 
 
-def test_forward_deterministic():
+@pytest.mark.parametrize("spec,L", [(si.TINY, 96), (MID_SPLIT, 256)], ids=lambda v: getattr(v, "name", str(v)))
+def test_forward_deterministic(spec, L):
+    """Bitwise repeatable, also through the split-K partials (folded in split order)."""
     require_gpu()
     from paper_2608_11235_amd import Model
-    tokens = to_dev(si.prompt_tokens(3, 2, 96, si.TINY.vocab, si.TINY.mask_id))
-    with Model(si.TINY, seed=0, max_batch=2, max_seq=96) as m:
-        a = m.forward_logits(tokens, 0, 96).clone()
-        b = m.forward_logits(tokens, 0, 96).clone()
-    assert torch.equal(a, b)
+    tokens = to_dev(si.prompt_tokens(3, 2, L, spec.vocab, spec.mask_id))
+    with Model(spec, seed=0, max_batch=2, max_seq=L) as m:
+        runs = [m.forward_logits(tokens, 0, L).clone() for _ in range(4)]
+    for r in runs[1:]:
+        assert torch.equal(runs[0], r)
