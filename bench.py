@@ -36,8 +36,8 @@ TIME_EVERY = 4              # gate/up event timing on every 4th timed pass
 # file and the shared device headers.
 SHARED_SOURCES = ("paper_2608_11235_amd/csrc/common.hpp", "paper_2608_11235_amd/csrc/internal.hpp")
 COUNTER_TRAFFIC = {
-    "gate_up": ("paper_2608_11235_amd/csrc/gemm.hip", "3d648d2cf93dfec1", 247607842),
-    "vocab_gate": ("paper_2608_11235_amd/csrc/vocab_gate.hip", "811bb73db6a53c1f", 1036531363),
+    "gate_up": ("paper_2608_11235_amd/csrc/gemm.hip", "1325414ec2926977", 247623848),
+    "vocab_gate": ("paper_2608_11235_amd/csrc/vocab_gate.hip", "5f109193b36f8a66", 1036531376),
 }
 
 
