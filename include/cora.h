@@ -141,7 +141,11 @@ typedef struct cora_model cora_model;
  * weights are 1.  The LM head is also kept in a second, packed layout (the
  * order in which the few-row LM-head kernel streams it: 32-row groups of 1 KB
  * MFMA operand blocks), written once here: weight bytes include one more
- * V x d bf16 matrix.  Synchronous.  *out is set only on success. */
+ * V x d bf16 matrix.  Synchronous.  *out is set only on success.
+ * CORA_ERR_UNSUPPORTED when an activation matrix of max_batch x max_seq rows
+ * (fp32 residual rows, bf16 FFN or attention-head rows, max_seq rounded up to
+ * 64) would exceed 2 GB: the kernels address one with 32-bit byte offsets.
+ * CORA_ERR_OOM when the device allocation fails. */
 cora_status cora_model_create(const cora_model_cfg *cfg, uint64_t seed, int32_t max_batch,
                               int32_t max_seq, void *hip_stream, cora_model **out);
 cora_status cora_model_destroy(cora_model *model);

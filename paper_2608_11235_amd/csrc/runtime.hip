@@ -148,6 +148,17 @@ extern "C" cora_status cora_model_create(const cora_model_cfg* cfg, uint64_t see
   if (!cfg || !out) return fail(CORA_ERR_INVALID_ARG, "null cfg or out");
   if (cora_status st = validate_cfg(*cfg)) return st;
   if (max_batch <= 0 || max_seq <= 0) return fail(CORA_ERR_INVALID_ARG, "max_batch/max_seq <= 0");
+  if (max_batch > (1 << 24) || max_seq > (1 << 24))
+    return fail(CORA_ERR_UNSUPPORTED, "max_batch x max_seq too large: an activation matrix would exceed 2 GB");
+  {
+    // the GEMM operand loads address an activation matrix [max_batch * max_seq, width] with
+    // 32-bit byte offsets; bound the widest one (fp32 residual, bf16 FFN or head rows)
+    const size_t widest = std::max({(size_t)cfg->d_model * 4, (size_t)round_up(cfg->ffn_dim, 64) * 2,
+                                    (size_t)cfg->n_heads * cfg->head_dim * 2});
+    if ((size_t)max_batch * (size_t)round_up(max_seq, 64) * widest > 0x7fffffffULL)
+      return fail(CORA_ERR_UNSUPPORTED,
+                  "max_batch x max_seq too large: an activation matrix would exceed 2 GB");
+  }
   const hipStream_t s = S(hip_stream);
   cora_model* m = new cora_model();
   m->cfg = *cfg;

@@ -77,6 +77,19 @@ def test_create_rejects_bad_config(kw, status):
     assert lib.cora_last_error()
 
 
+@pytest.mark.parametrize("max_batch,max_seq", [(1 << 20, 64), (4096, 4096)])
+def test_create_rejects_oversized_workspace(max_batch, max_seq):
+    """Activation matrices beyond 2 GB (32-bit operand offsets) are refused before any
+    device call."""
+    lib, L = _lib()
+    cfg = _cfg(L)
+    h = ctypes.c_void_p()
+    st = lib.cora_model_create(ctypes.byref(cfg), 0, max_batch, max_seq, None, ctypes.byref(h))
+    assert st == -2
+    assert h.value is None
+    assert b"2 GB" in lib.cora_last_error()
+
+
 def test_vocab_gate_rejects_bad_arguments():
     lib, L = _lib()
     sc, gt = L.SchedCfg(32, 16), L.GateCfg(0.65, 1, 1, 0)
