@@ -21,11 +21,18 @@ cora_status fail(cora_status st, const std::string& msg) {
   return st;
 }
 
+// A failed HIP call is reported through the status alone: HIP's per-thread last-error
+// slot is cleared, so the caller's next hipGetLastError does not see it again.
+cora_status fail_hip(cora_status st, const std::string& msg) {
+  (void)hipGetLastError();
+  return fail(st, msg);
+}
+
 #define HIP_TRY(expr)                                                                   \
   do {                                                                                  \
     hipError_t e_ = (expr);                                                             \
     if (e_ != hipSuccess)                                                               \
-      return fail(CORA_ERR_HIP, std::string(#expr) + ": " + hipGetErrorString(e_));    \
+      return fail_hip(CORA_ERR_HIP, std::string(#expr) + ": " + hipGetErrorString(e_)); \
   } while (0)
 
 constexpr size_t ALIGN = 256;
@@ -210,13 +217,13 @@ extern "C" cora_status cora_model_create(const cora_model_cfg* cfg, uint64_t see
   hipError_t e = hipMalloc(&m->weight_mem, wb);
   if (e != hipSuccess) {
     cora_model_destroy(m);
-    return fail(e == hipErrorOutOfMemory ? CORA_ERR_OOM : CORA_ERR_HIP,
+    return fail_hip(e == hipErrorOutOfMemory ? CORA_ERR_OOM : CORA_ERR_HIP,
                 std::string("weight allocation: ") + hipGetErrorString(e));
   }
   e = hipMalloc(&m->ws_mem, wsb);
   if (e != hipSuccess) {
     cora_model_destroy(m);
-    return fail(e == hipErrorOutOfMemory ? CORA_ERR_OOM : CORA_ERR_HIP,
+    return fail_hip(e == hipErrorOutOfMemory ? CORA_ERR_OOM : CORA_ERR_HIP,
                 std::string("workspace allocation: ") + hipGetErrorString(e));
   }
   m->weight_bytes = wb;
@@ -276,7 +283,8 @@ extern "C" cora_status cora_model_create(const cora_model_cfg* cfg, uint64_t see
     e = hipHostMalloc((void**)&m->h_map, 3 * max_batch * sizeof(int32_t), hipHostMallocDefault);
   if (e != hipSuccess) {
     cora_model_destroy(m);
-    return fail(CORA_ERR_HIP, std::string("pinned allocation: ") + hipGetErrorString(e));
+    return fail_hip(e == hipErrorOutOfMemory ? CORA_ERR_OOM : CORA_ERR_HIP,
+                    std::string("pinned allocation: ") + hipGetErrorString(e));
   }
 
   // ---- fill weights
