@@ -59,13 +59,13 @@ def counter_traffic(name):
     return nbytes if digest is not None and source_digest(path) == digest else None
 
 
-def pass_flops(spec, M, rows):
+def pass_flops(spec, M, rows, batch=B):
     """Algorithmic FLOPs of one dense pass: GEMMs + attention + LM head on `rows` rows."""
     d, H, Hkv, hd, F, V = (spec.d_model, spec.n_heads, spec.n_kv_heads, spec.head_dim,
                            spec.ffn_dim, spec.vocab)
-    L = M // B
+    L = M // batch
     per_layer = 2 * M * d * (H + 2 * Hkv) * hd + 2 * M * H * hd * d + 2 * M * d * 2 * F \
-        + 2 * M * F * d + 4 * B * H * L * L * hd
+        + 2 * M * F * d + 4 * batch * H * L * L * hd
     return spec.n_layers * per_layer + 2 * rows * d * V
 
 
@@ -280,6 +280,44 @@ def compaction_leg(batch=8, logit_scale=8.0):
     return out
 
 
+def other_shapes_leg(passes=6, warmup=2):
+    """Labelled per-pass timing at the other two model shapes of the workload list: the
+    Dream-7B shape (GQA 28/4, QKV bias) at B = 8, L = 512, and the LLaDA-8B long canvas at
+    B = 1, L = 1280.  Each pass is one whole denoising step (dense pass, scores of the
+    active block rows, decision rules), timed by wall clock with no event stamps.  Not the
+    headline metric; the full long-run decode (1024 dense passes) is not timed here."""
+    import torch
+
+    import seeded_inputs as si
+    from paper_2608_11235_amd import DREAM_7B, LLADA_8B, DecodeState, Gate, Model, Sched
+
+    out = {}
+    for name, spec, b, p, g in (("dream7b_b8_gen256", DREAM_7B, 8, 256, 256),
+                                ("llada8b_long_gen1024", LLADA_8B, 1, 256, 1024)):
+        prompt = si.prompt_tokens(1, b, p, spec.vocab, spec.mask_id)
+        sched, gate = Sched(BLK, S), Gate(DELTA_P, M_REQ, True)
+        with Model(spec, seed=0, max_batch=b, max_seq=p + g) as m:
+            st = DecodeState.from_host(si.initial_decode_state(prompt, g, spec.mask_id), p, g,
+                                       BLK, BLK, device="cuda")
+            for _ in range(warmup):
+                m.denoise_step(st, sched, gate)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for _ in range(passes):
+                m.denoise_step(st, sched, gate)
+            torch.cuda.synchronize()
+            dt = (time.perf_counter() - t0) / passes
+        fl = pass_flops(spec, b * (p + g), b * BLK, batch=b)
+        out[name] = {"batch": b, "prompt_len": p, "gen_len": g, "passes_timed": passes,
+                     "ms_per_pass": round(dt * 1e3, 3), "passes_per_s": round(1 / dt, 3),
+                     "dense_gen_tokens_per_s": round(b * BLK / S / dt, 3),
+                     "pass_tflop": round(fl / 1e12, 4),
+                     "pass_mfma_frac": round(fl / dt / 1e12 / PEAK_BF16_TFLOPS, 4)}
+        torch.cuda.empty_cache()
+        note(f"shape {name} done")
+    return out
+
+
 def copy_calibration(nbytes=1 << 30, iters=5):
     """A plain device-to-device copy of known size: reference for HBM byte counters."""
     import torch
@@ -311,7 +349,10 @@ def main():
                     help="skip the labelled logits-x8 gated-decode leg")
     ap.add_argument("--no-compaction", action="store_true",
                     help="skip the labelled B=8 batch-row compaction leg")
-    ap.add_argument("--only", choices=["all", "pass", "vocab", "copy", "gated", "compaction"],
+    ap.add_argument("--no-shapes", action="store_true",
+                    help="skip the labelled Dream-7B B=8 and LLaDA-8B L=1280 pass timings")
+    ap.add_argument("--only", choices=["all", "pass", "vocab", "copy", "gated", "compaction",
+                                       "shapes"],
                     default="all",
                     help="run one leg only (profiling runs): the timed passes, the vocab/gate "
                          "kernel, or a plain 1 GiB device copy that calibrates byte counters")
@@ -328,9 +369,12 @@ def main():
     if args.only == "compaction":
         print(json.dumps({"compaction_b8_logits_x8": compaction_leg()}), flush=True)
         return
+    if args.only == "shapes":
+        print(json.dumps({"other_shapes": other_shapes_leg()}), flush=True)
+        return
     if args.only == "pass":
         args.no_decode = args.no_vocab = args.no_cpu_baseline = args.no_gated = True
-        args.no_compaction = True
+        args.no_compaction = args.no_shapes = True
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (batch rows "
               "decode independently, so more GPUs shard rows with no collective)", file=sys.stderr)
@@ -435,6 +479,8 @@ def main():
     if not args.no_compaction:
         result["compaction_b8_logits_x8"] = compaction_leg()
         note("compaction leg done")
+    if not args.no_shapes:
+        result["other_shapes"] = other_shapes_leg()
     if not args.no_cpu_baseline:
         note("cpu baseline leg starts")
         import seeded_inputs as si_
