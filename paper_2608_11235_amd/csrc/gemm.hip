@@ -350,41 +350,73 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void k_gemm(GemmArgs g) {
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int e4 = 0; e4 < 4; ++e4) {
-          float x[4], partner[4];
+        for (int hf = 0; hf < 2; ++hf) {  // rows 8 e4 + .. of e4 = 2 hf, 2 hf + 1
+          float x[2][4], partner[2][4];
 #pragma unroll
-          for (int t = 0; t < 4; ++t) {
-            x[t] = acc[i][j][e4 * 4 + t] + bias;
-            partner[t] = __shfl_xor(x[t], 1, 64);
+          for (int u = 0; u < 2; ++u)
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+              x[u][t] = acc[i][j][(2 * hf + u) * 4 + t] + bias;
+              partner[u][t] = __shfl_xor(x[u][t], 1, 64);
+            }
+          if (!in) continue;
+          const int rbase = m0 + wm * TM * 32 + i * 32 + row_q + 16 * hf;
+          if (sec < 2) {
+            // the cos/sin loads of these 8 elements are issued before their first store: a
+            // load behind a store would also wait for that store
+            float cs[2][4], sn[2][4];
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+              const int row0 = rbase + 8 * u;
+              int pos = row0 - row0 / o.L * o.L;
+#pragma unroll
+              for (int t = 0; t < 4; ++t) {
+                if (row0 + t < g.M) {
+                  cs[u][t] = o.cos_t[pos * half + ii];
+                  sn[u][t] = o.sin_t[pos * half + ii];
+                }
+                if (++pos == o.L) pos = 0;
+              }
+            }
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+              const int row0 = rbase + 8 * u;
+              if (row0 >= g.M) continue;
+              int b = row0 / o.L, pos = row0 - b * o.L;
+#pragma unroll
+              for (int t = 0; t < 4; ++t) {
+                if (row0 + t >= g.M) break;
+                const float r = (pd & 1) ? x[u][t] * cs[u][t] + partner[u][t] * sn[u][t]
+                                         : x[u][t] * cs[u][t] - partner[u][t] * sn[u][t];
+                uint16_t* dst = sec == 0
+                                    ? o.q + ((int64_t)(b * o.n_heads + head) * o.Ls + pos) * hd
+                                    : o.k + ((int64_t)(b * o.n_kv_heads + head) * o.Ls + pos) * hd;
+                dst[pd] = (uint16_t)f32_to_bf16_bits(r);
+                if (++pos == o.L) { pos = 0; ++b; }
+              }
+            }
+            continue;
           }
-          const int row0 = m0 + wm * TM * 32 + i * 32 + 8 * e4 + row_q;
-          if (!in || row0 >= g.M) continue;
-          int b = row0 / o.L, pos = row0 - b * o.L;
-          if (sec == 2 && pos + 3 < o.L && row0 + 3 < g.M) {
-            u32x2_t v2;
-            v2.x = pack_bf16x2(x[0], x[1]);
-            v2.y = pack_bf16x2(x[2], x[3]);
-            if ((o.L & 3) == 0) {
+#pragma unroll
+          for (int u = 0; u < 2; ++u) {
+            const int row0 = rbase + 8 * u;
+            if (row0 >= g.M) continue;
+            int b = row0 / o.L, pos = row0 - b * o.L;
+            if (pos + 3 < o.L && row0 + 3 < g.M && (o.L & 3) == 0) {
+              u32x2_t v2;
+              v2.x = pack_bf16x2(x[u][0], x[u][1]);
+              v2.y = pack_bf16x2(x[u][2], x[u][3]);
               *reinterpret_cast<u32x2_t*>(
                   &o.vt[((int64_t)(b * o.n_kv_heads + head) * hd + pd) * o.Ls + pos]) = v2;
               continue;
             }
-          }
 #pragma unroll
-          for (int t = 0; t < 4; ++t) {
-            if (row0 + t >= g.M) break;
-            if (sec < 2) {
-              const float c = o.cos_t[pos * half + ii], sn = o.sin_t[pos * half + ii];
-              const float r = (pd & 1) ? x[t] * c + partner[t] * sn : x[t] * c - partner[t] * sn;
-              uint16_t* dst = sec == 0
-                                  ? o.q + ((int64_t)(b * o.n_heads + head) * o.Ls + pos) * hd
-                                  : o.k + ((int64_t)(b * o.n_kv_heads + head) * o.Ls + pos) * hd;
-              dst[pd] = (uint16_t)f32_to_bf16_bits(r);
-            } else {
+            for (int t = 0; t < 4; ++t) {
+              if (row0 + t >= g.M) break;
               o.vt[((int64_t)(b * o.n_kv_heads + head) * hd + pd) * o.Ls + pos] =
-                  (uint16_t)f32_to_bf16_bits(x[t]);
+                  (uint16_t)f32_to_bf16_bits(x[u][t]);
+              if (++pos == o.L) { pos = 0; ++b; }
             }
-            if (++pos == o.L) { pos = 0; ++b; }
           }
         }
     }

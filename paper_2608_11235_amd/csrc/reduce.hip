@@ -157,19 +157,40 @@ __global__ __launch_bounds__(256) void k_qkv_finish(const float* __restrict__ pa
     }
     return;
   }
+  if (sec < 2) {
+    // every row's cos/sin loads are issued before the first store: a load behind a store
+    // would wait for that store too
+    int bt[4], pt[4];
+    float2 cs[4], sn[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      bt[t] = b;
+      pt[t] = pos;
+      if (t < nr) {
+        cs[t] = *reinterpret_cast<const float2*>(o.cos_t + pos * half + (pd >> 1));
+        sn[t] = *reinterpret_cast<const float2*>(o.sin_t + pos * half + (pd >> 1));
+      }
+      if (++pos == o.L) {
+        pos = 0;
+        ++b;
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      if (t >= nr) break;
+      u32x2_t q;
+      q.x = pack_bf16x2(x[t][0] * cs[t].x - x[t][1] * sn[t].x, x[t][1] * cs[t].x + x[t][0] * sn[t].x);
+      q.y = pack_bf16x2(x[t][2] * cs[t].y - x[t][3] * sn[t].y, x[t][3] * cs[t].y + x[t][2] * sn[t].y);
+      uint16_t* dst = sec == 0 ? o.q + ((int64_t)(bt[t] * o.n_heads + head) * o.Ls + pt[t]) * hd
+                               : o.k + ((int64_t)(bt[t] * o.n_kv_heads + head) * o.Ls + pt[t]) * hd;
+      *reinterpret_cast<u32x2_t*>(dst + pd) = q;
+    }
+    return;
+  }
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
     if (t >= nr) break;
-    if (sec < 2) {
-      const float2 cs = *reinterpret_cast<const float2*>(o.cos_t + pos * half + (pd >> 1));
-      const float2 sn = *reinterpret_cast<const float2*>(o.sin_t + pos * half + (pd >> 1));
-      u32x2_t q;
-      q.x = pack_bf16x2(x[t][0] * cs.x - x[t][1] * sn.x, x[t][1] * cs.x + x[t][0] * sn.x);
-      q.y = pack_bf16x2(x[t][2] * cs.y - x[t][3] * sn.y, x[t][3] * cs.y + x[t][2] * sn.y);
-      uint16_t* dst = sec == 0 ? o.q + ((int64_t)(b * o.n_heads + head) * o.Ls + pos) * hd
-                               : o.k + ((int64_t)(b * o.n_kv_heads + head) * o.Ls + pos) * hd;
-      *reinterpret_cast<u32x2_t*>(dst + pd) = q;
-    } else {
+    {
       uint16_t* dst = o.vt + ((int64_t)(b * o.n_kv_heads + head) * hd + pd) * o.Ls + pos;
 #pragma unroll
       for (int j = 0; j < 4; ++j) dst[j * o.Ls] = (uint16_t)f32_to_bf16_bits(x[t][j]);
