@@ -112,7 +112,22 @@ class _RandomModel:
                                                  (0.0, 1, True), (0.65, 1, False)])
 def test_decode_invariants(seed, delta_p, m_req, gate, scope):
     """(0.0, 1) is the persistence-only variant, (0.3, 0) confidence-only, m = 2 two checks."""
-    V, P, G, blk, S = 23, 5, 24, 8, 4
+    _check_decode_invariants(seed, delta_p, m_req, gate, scope, 23, 5, 24, 8, 4)
+
+
+@pytest.mark.parametrize("scope", ["block", "global"])
+@pytest.mark.parametrize("seed", range(2))
+@pytest.mark.parametrize("delta_p,m_req,gate", [(0.65, 1, True), (0.3, 0, True), (0.5, 2, True),
+                                                 (0.0, 1, True), (0.65, 1, False)])
+@pytest.mark.parametrize("P,G,blk,S", [(0, 24, 8, 4),     # empty prompt
+                                       (5, 6, 1, 1),      # one-position blocks
+                                       (3, 32, 32, 32),   # one block, one transfer per step
+                                       (2, 16, 16, 3)])   # k_s = 6, 5, 5
+def test_decode_invariants_degenerate_shapes(seed, delta_p, m_req, gate, scope, P, G, blk, S):
+    _check_decode_invariants(seed, delta_p, m_req, gate, scope, 23, P, G, blk, S)
+
+
+def _check_decode_invariants(seed, delta_p, m_req, gate, scope, V, P, G, blk, S):
     mask_id = V - 1
     model = _RandomModel(V, P + G, seed, scale=1.5)
     prompt = np.random.default_rng(100 + seed).integers(0, V - 1, (2, P))
