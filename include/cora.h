@@ -22,6 +22,11 @@
  *  - Work is enqueued on the caller's HIP stream (`hip_stream`, a hipStream_t;
  *    NULL = the default stream) in stream order.  Only cora_block_decode and
  *    cora_model_copy_tensor wait on the host.
+ *  - Every call on one model uses that model's single workspace (activations,
+ *    logits or score partials, split-K partials, decode state of
+ *    cora_block_decode).  Calls on one model must therefore not overlap: issue
+ *    them from one host thread at a time and on one stream, or order the
+ *    streams.  Different models are independent.
  *  - Shapes are validated up front; unsupported shapes return
  *    CORA_ERR_UNSUPPORTED, malformed arguments CORA_ERR_INVALID_ARG, HIP
  *    failures CORA_ERR_HIP (with hipGetErrorString text in cora_last_error()).
