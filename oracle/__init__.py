@@ -18,6 +18,8 @@ theory   : Proposition 1 (margin condition and its confidence bound),
 
 Every function cites the passage it follows.  Parity pins live in
 ``tests/test_oracle_*.py``.  Readings of points the paper leaves open are
-listed in the design doc and named in the code as R-numbers.
+stated where they are applied: the decision rules' readings, numbered R1-R27,
+in the ``decode`` docstring; the backbone the paper does not spell out in the
+``forward`` docstring.
 """
 from . import forward, decode, theory  # noqa: F401

@@ -12,7 +12,7 @@ State arrays (per batch row b, canvas position i):
     block_idx[b]      active generation block (== n_blocks once finished)
     step_idx[b]       executed steps so far in the active block
 
-Readings of points the paper leaves open (the R-numbers of the design doc):
+Readings of points the paper leaves open, numbered as in the rest of the oracle:
     R1  k_s: linear split of the block's M masked positions over S_b steps,
         k_s = floor(M / S_b) + [s < M mod S_b], fixed at block start.
     R2  the transfer rule takes the k_s highest-confidence positions of the

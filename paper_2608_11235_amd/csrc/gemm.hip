@@ -36,6 +36,10 @@
 //                         same outputs: C = bf16(silu(g) * u), ldc over ffn columns.
 //             EPI_QKV_ROPE  bias, rotate-half RoPE on q and k, head-major q/k and
 //                         transposed v written straight from the accumulators.
+//             EPI_TOP1    no C: per row and wavefront column range, (max, first arg max,
+//                         sum of exp) of the bf16 logits EPI_BF16 would store (Eq. 1).
+// Weights are either row-major or stored in 64 x 64 blocks (w_packed), in which case a
+// tile's BK-slice of W is a run of whole 8 KB blocks.
 // Requirements: K % (64 * splits) == 0; M, N arbitrary (tails clamped on load, masked
 // on store).
 #include <hip/hip_ext.h>

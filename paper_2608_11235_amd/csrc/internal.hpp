@@ -5,7 +5,7 @@
 
 namespace cora {
 
-// ---- weight init (K10) ------------------------------------------------------------------
+// ---- weight init ------------------------------------------------------------------------
 // Physical row of logical row r: 0 identity (+row_offset), 1 gate half and 2 up half of
 // the 32-row interleaved gate/up matrix.
 // 3: rows of q or k heads stored pair-interleaved within each head of hd rows (logical
@@ -141,7 +141,7 @@ hipError_t launch_attention(const uint16_t* q, const uint16_t* k, const uint16_t
                             uint16_t* out, int B, int L, int Ls, int H, int Hkv, int hd,
                             int num_cus, hipStream_t s);
 
-// ---- vocab / gate (K9) -------------------------------------------------------------------
+// ---- vocab / gate -------------------------------------------------------------------------
 // Logits rows r of batch row b (row-major [B, n_rows, V]) score canvas position
 // row_begin + r (row_begin >= 0) or lo_b + r (row_begin < 0, lo_b = active block start).
 // Their top-1 / confidence go to top1/conf[b * out_ld + out_off + r], so a region can be
