@@ -1,4 +1,7 @@
-// Vocab reduction + decision rules: two launches per denoising step.
+// Vocab reduction over logits rows, and the decision rules.  A denoising step computes
+// Eq. (1) inside its LM-head pass and runs only k_gate_rules from here; k_vocab_top1
+// reduces logits a caller hands over (cora_vocab_gate), and the rows of a step whose
+// vocabulary is too small to hold the fused pass's partials in the logits buffer.
 //
 // k_vocab_top1, one workgroup per logits row: a single coalesced pass over the bf16 row
 // (16-byte streaming loads, the next group of four in flight while the current one is
