@@ -36,8 +36,8 @@ TIME_EVERY = 4              # gate/up event timing on every 4th timed pass
 # file and the shared device headers.
 SHARED_SOURCES = ("paper_2608_11235_amd/csrc/common.hpp", "paper_2608_11235_amd/csrc/internal.hpp")
 COUNTER_TRAFFIC = {
-    "gate_up": ("paper_2608_11235_amd/csrc/gemm.hip", "fcd961575fa61f7b", 247626183),
-    "vocab_gate": ("paper_2608_11235_amd/csrc/vocab_gate.hip", "5f109193b36f8a66", 1036531376),
+    "gate_up": ("paper_2608_11235_amd/csrc/gemm.hip", "0cdb3f7932e7f020", 247624972),
+    "vocab_gate": ("paper_2608_11235_amd/csrc/vocab_gate.hip", "b83e656124978083", 1036531324),
 }
 
 
