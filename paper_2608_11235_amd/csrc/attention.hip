@@ -7,8 +7,12 @@
 // the second half of the key tiles, and the two partial softmax states (max, sum, O) are
 // merged through LDS at the end.  Small grids (B * H * L / 64 below two workgroups per CU)
 // use SPLIT = 2, which doubles the wavefronts per SIMD and halves each one's serial chain.
-// Key tiles of 64 are staged in LDS, double buffered: the next tile's loads are in flight
-// in registers while the current tile is multiplied out of LDS (one barrier per tile).
+// Key tiles of 64 are staged in LDS: the next tile's loads are in flight in registers while
+// the current tile is multiplied out of LDS.  Small grids double-buffer the tile (one
+// barrier per tile).  Large grids (SB) keep one LDS tile buffer and at most 168 registers,
+// so three workgroups share a CU (three wavefronts per SIMD instead of two): each
+// wavefront's per-tile chain (MFMAs, max, lane exchange, exp, MFMAs) is latency-bound, and
+// the third wavefront hides more of it than the second barrier per tile costs.
 // Softmax terms use the hardware v_exp_f32 (arguments <= 0; results below 2^-126 flush to
 // zero, which no sum holding its max term can notice).
 // Everything is computed transposed with v_mfma_f32_16x16x32_bf16 so that a query's
@@ -23,8 +27,8 @@
 
 namespace cora {
 
-template <int HD, int SPLIT>
-__global__ __launch_bounds__(256 * SPLIT) void k_attention(const uint16_t* __restrict__ q,
+template <int HD, int SPLIT, bool SB = false>
+__global__ __launch_bounds__(256 * SPLIT, SB ? 3 : 1) void k_attention(const uint16_t* __restrict__ q,
                                                    const uint16_t* __restrict__ k,
                                                    const uint16_t* __restrict__ vt,
                                                    uint16_t* __restrict__ out, int L, int Ls,
@@ -33,8 +37,9 @@ __global__ __launch_bounds__(256 * SPLIT) void k_attention(const uint16_t* __res
   constexpr int LDKS = HD + 8;    // padded LDS rows
   constexpr int LDVS = KT + 8;
   constexpr int CK = KT * HD / 8 / 256;  // 16-byte chunks per thread per tile (K and V^T each)
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][SPLIT][KT * LDKS];
-  __shared__ __attribute__((aligned(16))) uint16_t Vs[2][SPLIT][HD * LDVS];
+  constexpr int NB = SB ? 1 : 2;  // LDS tile buffers
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[NB][SPLIT][KT * LDKS];
+  __shared__ __attribute__((aligned(16))) uint16_t Vs[NB][SPLIT][HD * LDVS];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int part = wave >> 2;                // which part of the key range
@@ -60,19 +65,17 @@ __global__ __launch_bounds__(256 * SPLIT) void k_attention(const uint16_t* __res
   // K tile [64 keys][HD] and V^T tile [HD][64 keys] of part tpart: chunk c of this thread
   // (pointers of key 0; a tile adds the uniform key0 * HD / key0)
   u32x4_t rk[CK], rv[CK];
-  const uint16_t* kp[CK];
-  const uint16_t* vp[CK];
-#pragma unroll
-  for (int i = 0; i < CK; ++i) {
-    const int c = tl + i * 256;
-    kp[i] = kh + (c / (HD / 8)) * HD + (c % (HD / 8)) * 8;
-    vp[i] = vh + (int64_t)(c / (KT / 8)) * Ls + (c % (KT / 8)) * 8;
-  }
+  // chunk i of this thread: K row tl / (HD/8) + i * (256 / (HD/8)), V^T row tl / (KT/8) +
+  // i * (256 / (KT/8)); one lane offset per tensor, the rest uniform strides
+  const int koff = (tl / (HD / 8)) * HD + (tl % (HD / 8)) * 8;
+  const int voff = (tl / (KT / 8)) * Ls + (tl % (KT / 8)) * 8;
   auto fetch = [&](int key0) {
+    const uint16_t* kb0 = kh + (int64_t)key0 * HD + koff;
+    const uint16_t* vb0 = vh + key0 + voff;
 #pragma unroll
     for (int i = 0; i < CK; ++i) {
-      rk[i] = *reinterpret_cast<const u32x4_t*>(kp[i] + (int64_t)key0 * HD);
-      rv[i] = *reinterpret_cast<const u32x4_t*>(vp[i] + key0);
+      rk[i] = *reinterpret_cast<const u32x4_t*>(kb0 + i * (256 / (HD / 8)) * HD);
+      rv[i] = *reinterpret_cast<const u32x4_t*>(vb0 + (int64_t)i * (256 / (KT / 8)) * Ls);
     }
   };
   // K rows are stored in a permuted key order: tile key k = 32 a + 8 g + 4 b + i (a, b in
@@ -101,7 +104,7 @@ __global__ __launch_bounds__(256 * SPLIT) void k_attention(const uint16_t* __res
   stash(0);
   __syncthreads();
   for (int j = 0; j < per; ++j) {
-    const int buf = j & 1, kt = part * per + j, key0 = kt * KT;
+    const int buf = SB ? 0 : (j & 1), kt = part * per + j, key0 = kt * KT;
     const int next = tpart * per + j + 1;  // this thread's next tile to load
     if (j + 1 < per && next < n_tiles) fetch(next * KT);  // in flight during this tile
     if (kt < n_tiles) {
@@ -168,7 +171,10 @@ __global__ __launch_bounds__(256 * SPLIT) void k_attention(const uint16_t* __res
         }
       }
     }
-    if (j + 1 < per) stash(buf ^ 1);
+    if (j + 1 < per) {
+      if constexpr (SB) __syncthreads();  // one buffer: every wavefront is done with tile j
+      stash(SB ? 0 : buf ^ 1);
+    }
     __syncthreads();
   }
 
@@ -222,15 +228,15 @@ hipError_t launch_attention(const uint16_t* q, const uint16_t* k, const uint16_t
   const float scale_log2 = 1.4426950408889634f / sqrtf((float)hd);
   const dim3 grid(Ls / 64, B * H);
   const bool split = (int64_t)grid.x * grid.y < 2 * (int64_t)num_cus;
-#define ATTN(HD_, SP_)                                                                     \
-  hipLaunchKernelGGL((k_attention<HD_, SP_>), grid, dim3(256 * SP_), 0, s, q, k, vt, out, L, \
+#define ATTN(HD_, SP_, SB_)                                                                \
+  hipLaunchKernelGGL((k_attention<HD_, SP_, SB_>), grid, dim3(256 * SP_), 0, s, q, k, vt, out, L, \
                      Ls, H, Hkv, scale_log2)
   if (hd == 128) {
-    if (split) ATTN(128, 2);
-    else ATTN(128, 1);
+    if (split) ATTN(128, 2, false);
+    else ATTN(128, 1, true);
   } else if (hd == 64) {
-    if (split) ATTN(64, 2);
-    else ATTN(64, 1);
+    if (split) ATTN(64, 2, false);
+    else ATTN(64, 1, true);
   } else {
     return hipErrorInvalidValue;
   }
