@@ -28,7 +28,7 @@
 namespace cora {
 
 template <int HD, int SPLIT, bool SB = false>
-__global__ __launch_bounds__(256 * SPLIT, SB ? 3 : 1) void k_attention(const uint16_t* __restrict__ q,
+__global__ __launch_bounds__(256 * SPLIT, SB && SPLIT == 1 ? 3 : 1) void k_attention(const uint16_t* __restrict__ q,
                                                    const uint16_t* __restrict__ k,
                                                    const uint16_t* __restrict__ vt,
                                                    uint16_t* __restrict__ out, int L, int Ls,
@@ -38,8 +38,12 @@ __global__ __launch_bounds__(256 * SPLIT, SB ? 3 : 1) void k_attention(const uin
   constexpr int LDVS = KT + 8;
   constexpr int CK = KT * HD / 8 / 256;  // 16-byte chunks per thread per tile (K and V^T each)
   constexpr int NB = SB ? 1 : 2;  // LDS tile buffers
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[NB][SPLIT][KT * LDKS];
-  __shared__ __attribute__((aligned(16))) uint16_t Vs[NB][SPLIT][HD * LDVS];
+  // K tiles [NB][SPLIT][KT * LDKS], then V^T tiles [NB][SPLIT][HD * LDVS], in one region
+  // that the merge of the parts reuses after the last tile
+  constexpr int KSZ = KT * LDKS, VSZ = HD * LDVS;
+  __shared__ __attribute__((aligned(16))) uint16_t lds[NB * SPLIT * (KSZ + VSZ)];
+  auto Kt = [&](int buf, int p) { return lds + (buf * SPLIT + p) * KSZ; };
+  auto Vt = [&](int buf, int p) { return lds + NB * SPLIT * KSZ + (buf * SPLIT + p) * VSZ; };
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int part = wave >> 2;                // which part of the key range
@@ -89,9 +93,9 @@ __global__ __launch_bounds__(256 * SPLIT, SB ? 3 : 1) void k_attention(const uin
     for (int i = 0; i < CK; ++i) {
       const int c = tl + i * 256;
       const int kr = c / (HD / 8), kc = (c % (HD / 8)) * 8;
-      *reinterpret_cast<u32x4_t*>(&Ks[buf][tpart][krow(kr) * LDKS + kc]) = rk[i];
+      *reinterpret_cast<u32x4_t*>(Kt(buf, tpart) + krow(kr) * LDKS + kc) = rk[i];
       const int vr = c / (KT / 8), vc = (c % (KT / 8)) * 8;
-      *reinterpret_cast<u32x4_t*>(&Vs[buf][tpart][vr * LDVS + vc]) = rv[i];
+      *reinterpret_cast<u32x4_t*>(Vt(buf, tpart) + vr * LDVS + vc) = rv[i];
     }
   };
 
@@ -115,7 +119,7 @@ __global__ __launch_bounds__(256 * SPLIT, SB ? 3 : 1) void k_attention(const uin
 #pragma unroll
         for (int kk = 0; kk < HD / 32; ++kk) {
           const bf16x8_t a = as_bf16x8(
-              *reinterpret_cast<const u32x4_t*>(&Ks[buf][part][(kb * 16 + r16) * LDKS + kk * 32 + g * 8]));
+              *reinterpret_cast<const u32x4_t*>(Kt(buf, part) + (kb * 16 + r16) * LDKS + kk * 32 + g * 8));
           st[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[kk], st[kb], 0, 0, 0);
         }
       }
@@ -166,7 +170,7 @@ __global__ __launch_bounds__(256 * SPLIT, SB ? 3 : 1) void k_attention(const uin
 #pragma unroll
         for (int d = 0; d < HD / 16; ++d) {
           const u32x4_t av = *reinterpret_cast<const u32x4_t*>(
-              &Vs[buf][part][(d * 16 + r16) * LDVS + ks * 32 + g * 8]);
+              Vt(buf, part) + (d * 16 + r16) * LDVS + ks * 32 + g * 8);
           o[d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(av), bfrag, o[d], 0, 0, 0);
         }
       }
@@ -178,14 +182,14 @@ __global__ __launch_bounds__(256 * SPLIT, SB ? 3 : 1) void k_attention(const uin
     __syncthreads();
   }
 
-  if constexpr (SPLIT == 2) {
-    // merge the second part's (max, partial sums, O) into the first part's wavefronts;
-    // the K tiles' LDS is free after the loop's last barrier
+  if constexpr (SPLIT >= 2) {
+    // parts 1 .. SPLIT-1 hand their (max, partial sums, O) to part 0's wavefronts, which
+    // fold them in part order; the tiles' LDS is free after the loop's last barrier
     constexpr int NF = 2 + 4 * (HD / 16);
-    float* comb = reinterpret_cast<float*>(&Ks[0][0][0]);
-    static_assert(sizeof(Ks) >= 4 * NF * 64 * sizeof(float), "merge buffer");
-    const int slot = (wave & 3) * NF * 64 + lane;
-    if (part == 1) {
+    float* comb = reinterpret_cast<float*>(lds);
+    static_assert(sizeof(lds) >= (size_t)(SPLIT - 1) * 4 * NF * 64 * sizeof(float), "merge buffer");
+    if (part > 0) {
+      const int slot = ((part - 1) * 4 + (wave & 3)) * NF * 64 + lane;
       comb[slot] = m_run;
       comb[slot + 64] = l_part;
 #pragma unroll
@@ -194,15 +198,21 @@ __global__ __launch_bounds__(256 * SPLIT, SB ? 3 : 1) void k_attention(const uin
         for (int i = 0; i < 4; ++i) comb[slot + (2 + 4 * d + i) * 64] = o[d][i];
     }
     __syncthreads();
-    if (part == 1) return;
-    const float m1 = comb[slot], l1 = comb[slot + 64];
-    const float m = fmaxf(m_run, m1);
-    const float a0 = fast_exp2(m_run - m), a1 = fast_exp2(m1 - m);
-    l_part = l_part * a0 + l1 * a1;
+    if (part > 0) return;
 #pragma unroll
-    for (int d = 0; d < HD / 16; ++d)
+    for (int p = 1; p < SPLIT; ++p) {
+      const int slot = ((p - 1) * 4 + (wave & 3)) * NF * 64 + lane;
+      const float m1 = comb[slot], l1 = comb[slot + 64];
+      const float m = fmaxf(m_run, m1);
+      const float a0 = fast_exp2(m_run - m), a1 = fast_exp2(m1 - m);
+      m_run = m;
+      l_part = l_part * a0 + l1 * a1;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) o[d][i] = o[d][i] * a0 + comb[slot + (2 + 4 * d + i) * 64] * a1;
+      for (int d = 0; d < HD / 16; ++d)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          o[d][i] = o[d][i] * a0 + comb[slot + (2 + 4 * d + i) * 64] * a1;
+    }
   }
 
   float l = l_part;
