@@ -53,12 +53,9 @@ namespace cora {
 constexpr int BK = 64;
 constexpr int LDK = BK + 8;  // padded LDS row, in bf16 elements
 
-// n 16-byte loads at byte offset voff + i * step (step uniform) through a buffer resource
-// n 16-byte loads at byte offset voff + i * step (step uniform) through a buffer resource;
-// when the chunks do not divide evenly, the last one exists only for threads with
-// tid + (N-1) * NT < total.
-// n 16-byte loads, the last one from its own per-lane base (an out-of-range base makes the
-// hardware return zeros without touching memory)
+// N 16-byte loads at byte offsets voff + i * step (step uniform) through a buffer resource,
+// the last one from its own per-lane offset voff_last (an offset past the resource's range
+// makes the hardware return zeros without touching memory)
 template <int N>
 __device__ __forceinline__ void buf_load_tail(u32x4_t (&r)[N], __amdgpu_buffer_rsrc_t rs, int voff,
                                               int voff_last, int step) {
@@ -68,7 +65,7 @@ __device__ __forceinline__ void buf_load_tail(u32x4_t (&r)[N], __amdgpu_buffer_r
         u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, i + 1 < N ? voff : voff_last, i * step, 0));
 }
 
-// n 16-byte loads at per-chunk byte offsets voff[i] + koff (koff uniform); when the chunks
+// N 16-byte loads at per-chunk byte offsets voff[i] + koff (koff uniform); when the chunks
 // do not divide evenly and EXACT is false, the last one only where last_ok
 template <int N, bool EXACT>
 __device__ __forceinline__ void buf_load_chunks(u32x4_t (&r)[N], __amdgpu_buffer_rsrc_t rs,
@@ -79,6 +76,8 @@ __device__ __forceinline__ void buf_load_chunks(u32x4_t (&r)[N], __amdgpu_buffer
       r[i] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, voff[i] + koff, 0, 0));
 }
 
+// N 16-byte loads at byte offsets voff + i * step (step uniform); when the chunks do not
+// divide evenly and EXACT is false, the last one only where last_ok
 template <int N, bool EXACT>
 __device__ __forceinline__ void buf_load(u32x4_t (&r)[N], __amdgpu_buffer_rsrc_t rs, int voff,
                                          int step, bool last_ok) {
