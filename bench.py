@@ -36,7 +36,7 @@ TIME_EVERY = 4              # gate/up event timing on every 4th timed pass
 # file and the shared device headers.
 SHARED_SOURCES = ("paper_2608_11235_amd/csrc/common.hpp", "paper_2608_11235_amd/csrc/internal.hpp")
 COUNTER_TRAFFIC = {
-    "gate_up": ("paper_2608_11235_amd/csrc/gemm.hip", "0cdb3f7932e7f020", 247624972),
+    "gate_up": ("paper_2608_11235_amd/csrc/gemm.hip", "f98a384cb63fd75d", 247624449),
     "vocab_gate": ("paper_2608_11235_amd/csrc/vocab_gate.hip", "b83e656124978083", 1036531324),
 }
 
