@@ -233,12 +233,13 @@ cora_status cora_model_copy_tensor(cora_model *model, int32_t tensor_id, void *h
  * time (ms) and the number of timed launches since the previous read, and
  * clears both. */
 cora_status cora_model_set_timing(cora_model *model, int32_t enable);
+cora_status cora_model_read_timing(cora_model *model, double *total_ms, int64_t *launches);
+
 /* Batch-row compaction in cora_block_decode (R15: rows decode independently, so
  * dropping finished rows from the dense pass changes no live row's inputs; row
  * results can differ only in rounding where a kernel's split of the work
  * depends on the row count).  enable != 0 turns it on (default), 0 off. */
 cora_status cora_model_set_compaction(cora_model *model, int32_t enable);
-cora_status cora_model_read_timing(cora_model *model, double *total_ms, int64_t *launches);
 
 /* Device bytes the model holds (weights + workspace). */
 cora_status cora_model_device_bytes(cora_model *model, size_t *weight_bytes, size_t *workspace_bytes);
