@@ -15,6 +15,25 @@ _LAYER_SLOTS = {"wq": 0, "wk": 1, "wv": 2, "wo": 3, "wg": 4, "wu": 5, "wd": 6,
                 "bq": 7, "bk": 8, "bv": 9}
 
 
+_BF16_BITS = (torch.int16, torch.bfloat16, torch.uint16)
+
+
+def check_device_tensor(t, name, dtypes, numel=None):
+    """Refuse what the C ABI would misread: a host or non-contiguous tensor, another element
+    type, or fewer elements than the call reads or writes (the library sees only a pointer)."""
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name}: expected a torch.Tensor, got {type(t).__name__}")
+    if not t.is_cuda:
+        raise ValueError(f"{name}: must be a GPU tensor (got device {t.device})")
+    if t.dtype not in dtypes:
+        raise TypeError(f"{name}: dtype {t.dtype}, expected one of {dtypes}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name}: must be contiguous")
+    if numel is not None and t.numel() < numel:
+        raise ValueError(f"{name}: {t.numel()} elements, the call needs {numel}")
+    return t
+
+
 def layer_tensor_id(layer: int, name: str) -> int:
     return 100 + 16 * layer + _LAYER_SLOTS[name]
 
@@ -92,6 +111,16 @@ class DecodeState:
         return out
 
     def c(self):
+        B, L = self.B, self.prompt_len + self.gen_len
+        for name, dt, n in (("tokens", torch.int32, B * L), ("unresolved", torch.uint8, B * L),
+                            ("prev_top1", torch.int32, B * L), ("persist", torch.int32, B * L),
+                            ("block_idx", torch.int32, B), ("step_idx", torch.int32, B),
+                            ("top1", torch.int32, None), ("conf", torch.float32, None),
+                            ("decision", torch.uint8, None), ("done", torch.int32, B)):
+            check_device_tensor(getattr(self, name), f"state.{name}", (dt,), n)
+        if self.passes is not None:
+            check_device_tensor(self.passes, "state.passes", (torch.int32,),
+                                B * (self.gen_len // self.block_len))
         return _lib.State(ptr(self.tokens), ptr(self.unresolved), ptr(self.prev_top1),
                           ptr(self.persist), ptr(self.block_idx), ptr(self.step_idx),
                           ptr(self.top1), ptr(self.conf), ptr(self.decision), ptr(self.done),
@@ -132,10 +161,12 @@ class Model:
         return self._h
 
     def forward_logits(self, tokens, row_begin, n_rows, out=None, stream=None):
+        check_device_tensor(tokens, "tokens", (torch.int32,))
         B, L = tokens.shape
         if out is None:
             out = torch.empty((B, n_rows, self.spec.vocab), dtype=torch.int16,
                               device=tokens.device)
+        check_device_tensor(out, "out", _BF16_BITS, B * n_rows * self.spec.vocab)
         check(_lib.load().cora_forward_logits(self._h, ptr(tokens), B, L, row_begin, n_rows,
                                                ptr(out), stream_handle(stream)),
               "cora_forward_logits")
@@ -148,9 +179,11 @@ class Model:
               "cora_denoise_step")
 
     def block_decode(self, prompt, gen_len, sched: Sched, gate: Gate, out=None, stream=None):
+        check_device_tensor(prompt, "prompt", (torch.int32,))
         B, P = prompt.shape
         if out is None:
             out = torch.empty((B, P + gen_len), dtype=torch.int32, device=prompt.device)
+        check_device_tensor(out, "out", (torch.int32,), B * (P + gen_len))
         n_blocks = gen_len // sched.block_len
         passes = np.zeros((B, n_blocks), dtype=np.int32)
         total = ctypes.c_int32(0)
@@ -191,6 +224,7 @@ class Model:
 
 def vocab_gate(logits, n_rows, row_begin, V, mask_id, state: DecodeState, k_transfer,
                sched: Sched, gate: Gate, stream=None):
+    check_device_tensor(logits, "logits", _BF16_BITS, state.B * n_rows * V)
     st, sc, gt = state.c(), sched.c(), gate.c()
     check(_lib.load().cora_vocab_gate(ptr(logits), n_rows, row_begin, V, mask_id,
                                        ctypes.byref(st), k_transfer, ctypes.byref(sc),

@@ -66,3 +66,21 @@ def test_device_bytes():
     assert matrices <= w1 <= 3 * matrices
     assert w2 == w1
     assert 0 < ws1 < ws2
+
+
+def test_binding_refuses_misread_tensors():
+    require_gpu()
+    import torch
+    from paper_2608_11235_amd import Model
+    log_case("binding: wrong dtype, non-contiguous and undersized tensors refused")
+    with Model(SPEC, seed=0, max_batch=B, max_seq=P + G) as m:
+        tok = torch.zeros((B, P + G), dtype=torch.int32, device="cuda")
+        with pytest.raises(TypeError):
+            m.forward_logits(tok.long(), 0, 4)
+        with pytest.raises(ValueError, match="contiguous"):
+            m.forward_logits(torch.zeros((P + G, B), dtype=torch.int32, device="cuda").t(), 0, 4)
+        small = torch.empty((B, 3, SPEC.vocab), dtype=torch.int16, device="cuda")
+        with pytest.raises(ValueError, match="elements"):
+            m.forward_logits(tok, 0, 4, out=small)
+        m.forward_logits(tok, 0, 3, out=small)   # the right size goes through
+        torch.cuda.synchronize()
