@@ -11,7 +11,8 @@
  *
  * Conventions
  *  - Every function returns cora_status (0 = CORA_OK, < 0 = error) and never
- *    throws.  On error, cora_last_error() returns a thread-local message.  A
+ *    throws (a failed host allocation inside the library is CORA_ERR_OOM, and a
+ *    failed create frees whatever it had allocated).  On error, cora_last_error() returns a thread-local message.  A
  *    failed HIP call inside the library is reported through the status alone:
  *    HIP's last-error state is cleared before the function returns.
  *  - "d_" pointers are device pointers, "h_" pointers are host pointers.  All

@@ -7,6 +7,9 @@
 #include <algorithm>
 #include <vector>
 
+#include <new>
+#include <stdexcept>
+
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -16,9 +19,27 @@ namespace {
 
 thread_local std::string g_err;
 
-cora_status fail(cora_status st, const std::string& msg) {
-  g_err = msg;
+cora_status fail(cora_status st, const std::string& msg) noexcept {
+  try {
+    g_err = msg;
+  } catch (...) {
+    g_err.clear();
+  }
   return st;
+}
+
+// An exception escaping an entry point becomes a status (the C ABI never throws): host
+// allocation failure is CORA_ERR_OOM, anything else CORA_ERR_UNSUPPORTED with its text.
+cora_status exception_status() noexcept {
+  try {
+    throw;
+  } catch (const std::bad_alloc&) {
+    return fail(CORA_ERR_OOM, "host memory allocation failed");
+  } catch (const std::exception& x) {
+    return fail(CORA_ERR_UNSUPPORTED, std::string("unexpected C++ exception: ") + x.what());
+  } catch (...) {
+    return fail(CORA_ERR_UNSUPPORTED, "unexpected C++ exception");
+  }
 }
 
 // A failed HIP call is reported through the status alone: HIP's per-thread last-error
@@ -138,7 +159,7 @@ static hipStream_t S(void* s) { return reinterpret_cast<hipStream_t>(s); }
 // ---------------------------------------------------------------------------------------
 extern "C" const char* cora_last_error(void) { return g_err.c_str(); }
 
-extern "C" cora_status cora_model_destroy(cora_model* m) {
+extern "C" cora_status cora_model_destroy(cora_model* m) try {
   if (!m) return CORA_OK;
   for (hipEvent_t e : m->ev) (void)hipEventDestroy(e);
   if (m->h_block) (void)hipHostFree(m->h_block);
@@ -147,11 +168,13 @@ extern "C" cora_status cora_model_destroy(cora_model* m) {
   if (m->weight_mem) (void)hipFree(m->weight_mem);
   delete m;
   return CORA_OK;
+} catch (...) {
+  return exception_status();
 }
 
 extern "C" cora_status cora_model_create(const cora_model_cfg* cfg, uint64_t seed,
                                          int32_t max_batch, int32_t max_seq, void* hip_stream,
-                                         cora_model** out) {
+                                         cora_model** out) try {
   if (!cfg || !out) return fail(CORA_ERR_INVALID_ARG, "null cfg or out");
   if (cora_status st = validate_cfg(*cfg)) return st;
   if (max_batch <= 0 || max_seq <= 0) return fail(CORA_ERR_INVALID_ARG, "max_batch/max_seq <= 0");
@@ -168,6 +191,13 @@ extern "C" cora_status cora_model_create(const cora_model_cfg* cfg, uint64_t see
   }
   const hipStream_t s = S(hip_stream);
   cora_model* m = new cora_model();
+  // frees the partly built model on every failure path, including an exception
+  struct Guard {
+    cora_model* m;
+    ~Guard() {
+      if (m) cora_model_destroy(m);
+    }
+  } guard{m};
   m->cfg = *cfg;
   m->max_batch = max_batch;
   m->max_seq = max_seq;
@@ -216,13 +246,11 @@ extern "C" cora_status cora_model_create(const cora_model_cfg* cfg, uint64_t see
                align_up((size_t)max_batch * max_seq * 4) * 2 + align_up(3 * max_batch * 4);
   hipError_t e = hipMalloc(&m->weight_mem, wb);
   if (e != hipSuccess) {
-    cora_model_destroy(m);
     return fail_hip(e == hipErrorOutOfMemory ? CORA_ERR_OOM : CORA_ERR_HIP,
                 std::string("weight allocation: ") + hipGetErrorString(e));
   }
   e = hipMalloc(&m->ws_mem, wsb);
   if (e != hipSuccess) {
-    cora_model_destroy(m);
     return fail_hip(e == hipErrorOutOfMemory ? CORA_ERR_OOM : CORA_ERR_HIP,
                 std::string("workspace allocation: ") + hipGetErrorString(e));
   }
@@ -282,7 +310,6 @@ extern "C" cora_status cora_model_create(const cora_model_cfg* cfg, uint64_t see
   if (e == hipSuccess)
     e = hipHostMalloc((void**)&m->h_map, 3 * max_batch * sizeof(int32_t), hipHostMallocDefault);
   if (e != hipSuccess) {
-    cora_model_destroy(m);
     return fail_hip(e == hipErrorOutOfMemory ? CORA_ERR_OOM : CORA_ERR_HIP,
                     std::string("pinned allocation: ") + hipGetErrorString(e));
   }
@@ -330,18 +357,22 @@ extern "C" cora_status cora_model_create(const cora_model_cfg* cfg, uint64_t see
     return CORA_OK;
   }();
   if (st != CORA_OK) {
-    cora_model_destroy(m);
     return st;
   }
+  guard.m = nullptr;
   *out = m;
   return CORA_OK;
+} catch (...) {
+  return exception_status();
 }
 
-extern "C" cora_status cora_model_device_bytes(cora_model* m, size_t* wbytes, size_t* wsbytes) {
+extern "C" cora_status cora_model_device_bytes(cora_model* m, size_t* wbytes, size_t* wsbytes) try {
   if (!m) return fail(CORA_ERR_INVALID_ARG, "null model");
   if (wbytes) *wbytes = m->weight_bytes;
   if (wsbytes) *wsbytes = m->ws_bytes;
   return CORA_OK;
+} catch (...) {
+  return exception_status();
 }
 
 // ---- timing ------------------------------------------------------------------------------
@@ -356,20 +387,24 @@ static cora_status grow_events(cora_model* m, size_t n) {
   return CORA_OK;
 }
 
-extern "C" cora_status cora_model_set_compaction(cora_model* m, int32_t enable) {
+extern "C" cora_status cora_model_set_compaction(cora_model* m, int32_t enable) try {
   if (!m) return fail(CORA_ERR_INVALID_ARG, "null model");
   m->compaction = enable != 0;
   return CORA_OK;
+} catch (...) {
+  return exception_status();
 }
 
 // Turning timing on or off keeps what has been recorded; read_timing returns and clears it.
-extern "C" cora_status cora_model_set_timing(cora_model* m, int32_t enable) {
+extern "C" cora_status cora_model_set_timing(cora_model* m, int32_t enable) try {
   if (!m) return fail(CORA_ERR_INVALID_ARG, "null model");
   m->timing = enable != 0;
   // created up front so the timed passes do not pay for them
   if (m->timing)
     if (cora_status st = grow_events(m, 2 * m->layers.size() * 64)) return st;
   return CORA_OK;
+} catch (...) {
+  return exception_status();
 }
 
 static cora_status drain_events(cora_model* m) {
@@ -384,7 +419,7 @@ static cora_status drain_events(cora_model* m) {
   return CORA_OK;
 }
 
-extern "C" cora_status cora_model_read_timing(cora_model* m, double* total_ms, int64_t* launches) {
+extern "C" cora_status cora_model_read_timing(cora_model* m, double* total_ms, int64_t* launches) try {
   if (!m) return fail(CORA_ERR_INVALID_ARG, "null model");
   if (cora_status st = drain_events(m)) return st;
   if (total_ms) *total_ms = m->acc_ms;
@@ -392,6 +427,8 @@ extern "C" cora_status cora_model_read_timing(cora_model* m, double* total_ms, i
   m->acc_ms = 0.0;
   m->launches = 0;
   return CORA_OK;
+} catch (...) {
+  return exception_status();
 }
 
 // the next free (start, stop) event pair
@@ -567,7 +604,7 @@ static cora_status score_rows(cora_model* m, const RowSel& sel, int B, int n_row
 
 extern "C" cora_status cora_forward_logits(cora_model* m, const int32_t* d_tokens, int32_t B,
                                            int32_t L, int32_t row_begin, int32_t n_rows,
-                                           uint16_t* d_logits, void* hip_stream) {
+                                           uint16_t* d_logits, void* hip_stream) try {
   if (!m || !d_tokens || !d_logits) return fail(CORA_ERR_INVALID_ARG, "null argument");
   if (B <= 0 || L <= 0 || B > m->max_batch || L > m->max_seq)
     return fail(CORA_ERR_INVALID_ARG, "B/L outside [1, max_batch] x [1, max_seq]");
@@ -578,6 +615,8 @@ extern "C" cora_status cora_forward_logits(cora_model* m, const int32_t* d_token
   if (cora_status st = run_layers(m, d_tokens, B, L, s)) return st;
   const RowSel sel{1, L, n_rows, row_begin, 0, 0, 0, nullptr};
   return lm_head(m, sel, B * n_rows, d_logits, s);
+} catch (...) {
+  return exception_status();
 }
 
 // ---- decision rules ----------------------------------------------------------------------
@@ -630,7 +669,7 @@ static VocabGateArgs vg_args(const uint16_t* logits, int n_rows, int row_begin, 
 extern "C" cora_status cora_vocab_gate(const uint16_t* d_logits, int32_t n_rows, int32_t row_begin,
                                        int32_t V, int32_t mask_id, cora_state* st,
                                        int32_t k_transfer, const cora_sched_cfg* sc,
-                                       const cora_gate_cfg* gt, void* hip_stream) {
+                                       const cora_gate_cfg* gt, void* hip_stream) try {
   if (cora_status e = check_sched_gate(sc, gt)) return e;
   if (cora_status e = check_state(st, sc)) return e;
   if (!d_logits) return fail(CORA_ERR_INVALID_ARG, "null logits");
@@ -653,6 +692,8 @@ extern "C" cora_status cora_vocab_gate(const uint16_t* d_logits, int32_t n_rows,
   HIP_TRY(launch_vocab_top1(a, S(hip_stream)));
   HIP_TRY(launch_gate_rules(a, S(hip_stream)));
   return CORA_OK;
+} catch (...) {
+  return exception_status();
 }
 
 static cora_status denoise_step(cora_model* m, cora_state* st, const cora_sched_cfg* sc,
@@ -698,16 +739,18 @@ static cora_status check_step(cora_model* m, const cora_state* st, const cora_sc
 }
 
 extern "C" cora_status cora_denoise_step(cora_model* m, cora_state* st, const cora_sched_cfg* sc,
-                                         const cora_gate_cfg* gt, void* hip_stream) {
+                                         const cora_gate_cfg* gt, void* hip_stream) try {
   if (cora_status e = check_step(m, st, sc, gt)) return e;
   return denoise_step(m, st, sc, gt, S(hip_stream));
+} catch (...) {
+  return exception_status();
 }
 
 extern "C" cora_status cora_block_decode(cora_model* m, const int32_t* d_prompt, int32_t B,
                                          int32_t prompt_len, int32_t gen_len,
                                          const cora_sched_cfg* sc, const cora_gate_cfg* gt,
                                          int32_t* d_out_tokens, int32_t* h_passes,
-                                         int32_t* h_total_passes, void* hip_stream) {
+                                         int32_t* h_total_passes, void* hip_stream) try {
   if (!m || !d_out_tokens || !h_passes || (prompt_len > 0 && !d_prompt))
     return fail(CORA_ERR_INVALID_ARG, "null argument");
   const hipStream_t s = S(hip_stream);
@@ -778,6 +821,8 @@ extern "C" cora_status cora_block_decode(cora_model* m, const int32_t* d_prompt,
   HIP_TRY(hipStreamSynchronize(s));
   if (h_total_passes) *h_total_passes = (int32_t)total;
   return CORA_OK;
+} catch (...) {
+  return exception_status();
 }
 
 // ---- weight read-back in logical [out, in] layout ---------------------------------------
@@ -795,7 +840,7 @@ static cora_status read_packed(const uint16_t* d_packed, int64_t rows, int64_t l
 }
 
 extern "C" cora_status cora_model_copy_tensor(cora_model* m, int32_t tensor_id, void* h_dst,
-                                              size_t bytes) {
+                                              size_t bytes) try {
   if (!m || !h_dst) return fail(CORA_ERR_INVALID_ARG, "null argument");
   const auto& c = m->cfg;
   const int d = c.d_model;
@@ -872,4 +917,6 @@ extern "C" cora_status cora_model_copy_tensor(cora_model* m, int32_t tensor_id, 
     }
   }
   return fail(CORA_ERR_INVALID_ARG, "unknown tensor id");
+} catch (...) {
+  return exception_status();
 }
