@@ -73,48 +73,44 @@ def gu_flops(spec, M):
     return 2 * M * spec.d_model * 2 * spec.ffn_dim
 
 
-def cpu_baseline(spec, prompt, sample_layers=2, vocab_slice=16384):
-    """The oracle's dense pass on host cores, sampled: embedding + `sample_layers` of the
-    layers + the LM head over a `vocab_slice`-row slice of the vocabulary on the 32 block
-    rows, each part scaled to the full pass (layers x n_layers, LM head x V / slice)."""
+def cpu_baseline(spec, prompt):
+    """One whole dense pass of the oracle on host cores, unsampled, in fp32 (the oracle's
+    dtype parameter; numpy BLAS on every host thread): embedding, all layers at L = 512 and
+    the LM head on the 32 rows of the active block.  Weight generation (the seeded input) is
+    not timed; every step of the pass is."""
     import numpy as np
     from threadpoolctl import threadpool_info
 
     import seeded_inputs as si
     from oracle import forward as of
 
-    class _Slice:                      # LM head restricted to the first vocab_slice rows
-        def __init__(self, w, n):
-            self.final_norm, self._lm = w.final_norm, si.gen_rows(w.seed, si.TENSOR_LM_HEAD,
-                                                                  np.arange(n), spec.d_model)
-
-        def lm_head(self):
-            return self._lm
-
+    f32 = np.float32
     w = si.HostWeights(spec, 0, cache_layers=False)
     tokens = np.concatenate([prompt, np.full((1, G), spec.mask_id, np.int32)], axis=1)[0]
     L = tokens.shape[0]
-    cos, sin = of.rope_tables(L, spec.head_dim, spec.rope_theta, np.float64)
+    e = w.embed_rows(tokens)                           # input generation: not timed
     t0 = time.perf_counter()
-    h = np.asarray(w.embed_rows(tokens), dtype=np.float64)
-    t_embed = time.perf_counter() - t0
-    t_layers = 0.0
-    for i in range(sample_layers):
-        lw = w.layer(i)                              # input generation: not timed
+    cos, sin = of.rope_tables(L, spec.head_dim, spec.rope_theta, f32)
+    h = np.asarray(e, dtype=f32)
+    t_pass = time.perf_counter() - t0
+    for i in range(spec.n_layers):
+        lw = w.layer(i)                                # input generation: not timed
         t0 = time.perf_counter()
-        h = of.layer_forward(h, lw, spec, cos, sin, np.float64)
-        t_layers += time.perf_counter() - t0
-    sl = _Slice(w, vocab_slice)
+        h = of.layer_forward(h, lw, spec, cos, sin, f32)
+        t_pass += time.perf_counter() - t0
+        del lw
+        if i % 8 == 7:
+            note(f"cpu baseline: {i + 1} of {spec.n_layers} layers")
+    w.lm_head()                                        # input generation: not timed
     t0 = time.perf_counter()
-    of.logits_from_hidden(sl, spec, h[P:P + BLK], np.float64)
-    t_lm = (time.perf_counter() - t0) * spec.vocab / vocab_slice
-    t_pass = t_embed + t_layers / sample_layers * spec.n_layers + t_lm
+    of.logits_from_hidden(w, spec, h[P:P + BLK], f32)
+    t_pass += time.perf_counter() - t0
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    return {"value": 1.0 / t_pass, "unit": "passes/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"fp64 numpy oracle at L={L}: embedding + {sample_layers} of "
-                      f"{spec.n_layers} layers (scaled x{spec.n_layers / sample_layers:g}) + LM "
-                      f"head on {BLK} rows over {vocab_slice} of {spec.vocab} vocab rows (scaled); "
-                      f"{t_pass:.1f} s per full pass"}
+    return {"value": round(1.0 / t_pass, 5), "unit": "passes/s", "cores": int(threads),
+            "kind": "oracle", "nproc": os.cpu_count(),
+            "sample": f"one whole fp32 oracle pass at L={L}, unsampled: embedding, all "
+                      f"{spec.n_layers} layers, LM head on the {BLK} active-block rows; "
+                      f"{t_pass:.2f} s per pass"}
 
 
 def vocab_gate_roofline(iters=20):
@@ -148,14 +144,16 @@ def vocab_gate_roofline(iters=20):
             "workload": "bf16 logits [8, 512, 126464], k = 1"}
 
 
-def fidelity_run(m, prompt, gen_len, block_len, steps, delta_p, m_req, scope):
+def fidelity_run(m, prompt, gen_len, block_len, steps, delta_p, m_req, scope, dense=None):
     """Dense decode (gate off) and CORA decode (gate on, persistence scope `scope`) of the
     same prompts on model m, each timed by wall clock around cora_block_decode; then a
     step-by-step replay of the (deterministic) CORA decode that records every gate
     acceptance.  Returns executed passes, rho = CORA / dense passes, speedup, and the
     fidelity metrics against the dense endpoint: L^out, the fraction of generated
-    positions whose final token differs (Eq. 12), and L^acc, the fraction of gate-accepted
-    tokens that differ from the endpoint at their position (Eq. 7)."""
+    positions whose final token differs (Eq. 12), and L^acc (Eq. 7): per prompt, the
+    fraction of gate-accepted tokens that differ from the endpoint at their position (0 when
+    the gate accepted nothing), averaged over the prompts.  `dense` reuses the output of an
+    earlier dense decode of the same prompts (timed(...) below)."""
     import numpy as np
     import torch
 
@@ -173,7 +171,7 @@ def fidelity_run(m, prompt, gen_len, block_len, steps, delta_p, m_req, scope):
         dt = time.perf_counter() - t0
         return y.cpu().numpy(), passes, total, dt
 
-    y_d, p_d, tot_d, dt_d = timed(Gate(delta_p, m_req, False))
+    y_d, p_d, tot_d, dt_d = timed(Gate(delta_p, m_req, False)) if dense is None else dense
     gate = Gate(delta_p, m_req, True, scope)
     y, p, tot, dt = timed(gate)
     # replay, recording acceptances (decision 2) at the active block's positions
@@ -193,7 +191,8 @@ def fidelity_run(m, prompt, gen_len, block_len, steps, delta_p, m_req, scope):
                     pos = Pp + int(blk[b]) * block_len + int(j)
                     acc[b].append((pos, int(tok[b, pos])))
     n_acc = sum(len(a) for a in acc)
-    bad = sum(int(t != y_d[b, i]) for b in range(Bp) for i, t in acc[b])
+    bad = [sum(int(t != y_d[b, i]) for i, t in acc[b]) for b in range(Bp)]
+    l_acc = float(np.mean([bad[b] / len(acc[b]) if acc[b] else 0.0 for b in range(Bp)]))
     rho = float(p.sum()) / float(p_d.sum())
     return {
         "dense": {"passes": int(p_d.sum()), "wall_s": round(dt_d, 3),
@@ -202,10 +201,11 @@ def fidelity_run(m, prompt, gen_len, block_len, steps, delta_p, m_req, scope):
                  "inv_rho": round(1.0 / rho, 3), "wall_s": round(dt, 3),
                  "speedup_vs_dense": round(dt_d / dt, 3),
                  "L_out": float(np.mean(y[:, Pp:] != y_d[:, Pp:])), "accepted": n_acc,
-                 "L_acc": bad / n_acc if n_acc else 0.0,
+                 "L_acc": l_acc,
                  "replay_matches_block_decode": bool((st.tokens.cpu().numpy() == y).all())},
         "arrays": {"dense_tokens": y_d, "cora_tokens": y, "dense_passes": p_d, "cora_passes": p,
                    "accepted": acc},
+        "dense_run": (y_d, p_d, tot_d, dt_d),
     }
 
 
@@ -280,41 +280,95 @@ def compaction_leg(batch=8, logit_scale=8.0):
     return out
 
 
-def other_shapes_leg(passes=6, warmup=2):
-    """Labelled per-pass timing at the other two model shapes of the workload list: the
-    Dream-7B shape (GQA 28/4, QKV bias) at B = 8, L = 512, and the LLaDA-8B long canvas at
-    B = 1, L = 1280.  Each pass is one whole denoising step (dense pass, scores of the
-    active block rows, decision rules), timed by wall clock with no event stamps.  Not the
-    headline metric; the full long-run decode (1024 dense passes) is not timed here."""
+def shape_legs():
+    """The two other workloads: LLaDA-8B long fixed-horizon run (prompt 256 + gen 1024, 1024
+    steps, L = 1280) and Dream-7B at B = 8 (prompt 256 + gen 256, 256 steps)."""
+    import seeded_inputs as si
+    return {"llada8b_gen1024_decode": decode_leg("llada8b gen1024", si.LLADA_8B, 1, 256, 1024),
+            "dream7b_b8_gen256_decode": decode_leg("dream7b b8", si.DREAM_7B, 8, 256, 256)}
+
+
+def _timed_decode(m, pr, gen_len, sched, gate):
+    import torch
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    y, passes, total = m.block_decode(pr, gen_len, sched, gate)
+    torch.cuda.synchronize()
+    return y.cpu().numpy(), passes, total, time.perf_counter() - t0
+
+
+def decode_leg(name, spec, b, p, g):
+    """A whole gated block decode (gate (0.65, 1), BLOCK scope, batch-row compaction on) and
+    the dense fixed-horizon decode (gate off) of the same seeded prompts, each timed by wall
+    clock around cora_block_decode: executed passes (per block), the step ratio rho, time
+    per executed pass and generated tokens/s.  Random-init weights put every top-1
+    confidence near 1e-3, far below 0.65, so the gate accepts nothing and rho = 1 (reported
+    as measured)."""
+    import numpy as np
     import torch
 
     import seeded_inputs as si
-    from paper_2608_11235_amd import DREAM_7B, LLADA_8B, DecodeState, Gate, Model, Sched
+    from paper_2608_11235_amd import Gate, Model, Sched
 
-    out = {}
-    for name, spec, b, p, g in (("dream7b_b8_gen256", DREAM_7B, 8, 256, 256),
-                                ("llada8b_long_gen1024", LLADA_8B, 1, 256, 1024)):
-        prompt = si.prompt_tokens(1, b, p, spec.vocab, spec.mask_id)
-        sched, gate = Sched(BLK, S), Gate(DELTA_P, M_REQ, True)
-        with Model(spec, seed=0, max_batch=b, max_seq=p + g) as m:
-            st = DecodeState.from_host(si.initial_decode_state(prompt, g, spec.mask_id), p, g,
-                                       BLK, BLK, device="cuda")
-            for _ in range(warmup):
-                m.denoise_step(st, sched, gate)
-            torch.cuda.synchronize()
-            t0 = time.perf_counter()
-            for _ in range(passes):
-                m.denoise_step(st, sched, gate)
-            torch.cuda.synchronize()
-            dt = (time.perf_counter() - t0) / passes
-        fl = pass_flops(spec, b * (p + g), b * BLK, batch=b)
-        out[name] = {"batch": b, "prompt_len": p, "gen_len": g, "passes_timed": passes,
-                     "ms_per_pass": round(dt * 1e3, 3), "passes_per_s": round(1 / dt, 3),
-                     "dense_gen_tokens_per_s": round(b * BLK / S / dt, 3),
-                     "pass_tflop": round(fl / 1e12, 4),
-                     "pass_mfma_frac": round(fl / dt / 1e12 / PEAK_BF16_TFLOPS, 4)}
-        torch.cuda.empty_cache()
-        note(f"shape {name} done")
+    prompt = torch.from_numpy(si.prompt_tokens(1, b, p, spec.vocab, spec.mask_id)).cuda()
+    sched = Sched(BLK, S)
+    runs = {}
+    with Model(spec, seed=0, max_batch=b, max_seq=p + g) as m:
+        m.block_decode(prompt, BLK, sched, Gate(DELTA_P, M_REQ, True))  # warm-up: one block
+        for key, gate in (("cora", Gate(DELTA_P, M_REQ, True)),
+                          ("dense", Gate(DELTA_P, M_REQ, False))):
+            runs[key] = _timed_decode(m, prompt, g, sched, gate)
+            note(f"{name}: {key} decode {runs[key][2]} passes in {runs[key][3]:.1f} s")
+    fl = pass_flops(spec, b * (p + g), b * BLK, batch=b)
+    out = {"batch": b, "prompt_len": p, "gen_len": g, "block_len": BLK, "steps_per_block": S,
+           "total_steps": g // BLK * S, "gate": [DELTA_P, M_REQ], "pass_tflop": round(fl / 1e12, 4)}
+    for key, (y, passes, total, dt) in runs.items():
+        ms = dt / total * 1e3
+        out[key] = {"passes": int(passes.sum()), "batch_passes": int(total),
+                    "passes_per_block_row0": passes[0].tolist(), "wall_s": round(dt, 3),
+                    "ms_per_pass": round(ms, 3), "passes_per_s": round(total / dt, 3),
+                    "gen_tokens_per_s": round(b * g / dt, 3),
+                    "pass_mfma_frac": round(fl / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)}
+    out["rho"] = round(float(runs["cora"][1].sum()) / float(runs["dense"][1].sum()), 4)
+    out["tokens_equal_dense"] = bool((runs["cora"][0] == runs["dense"][0]).all())
+    out["note"] = ("random-init weights: top-1 confidence ~1e-3, so the gate never reaches "
+                   "0.65 and rho = 1")
+    torch.cuda.empty_cache()
+    return out
+
+
+def table3_sweep_leg(logit_scale=8.0):
+    """Labelled gate-variant sweep (the Table 3 ablation's settings; not a paper
+    configuration): the LLaDA-8B shape, batch 1, gen 256, logits x8 so the gate fires on
+    random weights.  One dense decode, then CORA with confidence only (m = 0), the default
+    (delta_p 0.65, m = 1), two checks (m = 2), persistence only (delta_p = 0, m = 1) and the
+    thresholds delta_p 0.5 and 0.8 (m = 1): rho, wall-clock speedup against 1/rho, L^acc
+    (Eq. 7, per-prompt mean) and L^out (Eq. 12)."""
+    from dataclasses import replace
+
+    import seeded_inputs as si
+    from paper_2608_11235_amd import LLADA_8B, Model
+
+    spec = replace(LLADA_8B, logit_scale=logit_scale, name=f"llada8b-logits-x{logit_scale:g}")
+    prompt = si.prompt_tokens(1, B, P, spec.vocab, spec.mask_id)
+    variants = (("m0", 0.65, 0), ("m1", 0.65, 1), ("m2", 0.65, 2), ("persistence_only", 0.0, 1),
+                ("dp0.5_m1", 0.5, 1), ("dp0.8_m1", 0.8, 1))
+    out = {"label": f"LLaDA-8B shape, B=1, gen 256, logits x{logit_scale:g} so the gate fires on "
+                    "random weights; the settings of the gate ablation, not a paper "
+                    "configuration", "scope": "block"}
+    dense = None
+    with Model(spec, seed=0, max_batch=B, max_seq=P + G) as m:
+        for name, dp, mr in variants:
+            r = fidelity_run(m, prompt, G, BLK, S, dp, mr, 0, dense=dense)
+            dense = r["dense_run"]
+            out["dense"] = r["dense"]
+            c = r["cora"]
+            out[name] = {"delta_p": dp, "m_req": mr, "passes": c["passes"], "rho": c["rho"],
+                         "speedup_vs_dense": c["speedup_vs_dense"],
+                         "speedup_over_inv_rho": round(c["speedup_vs_dense"] * c["rho"], 4),
+                         "L_acc": round(c["L_acc"], 4), "L_out": round(c["L_out"], 4),
+                         "accepted": c["accepted"]}
+            note(f"table-3 sweep: {name} rho {c['rho']}")
     return out
 
 
@@ -350,9 +404,12 @@ def main():
     ap.add_argument("--no-compaction", action="store_true",
                     help="skip the labelled B=8 batch-row compaction leg")
     ap.add_argument("--no-shapes", action="store_true",
-                    help="skip the labelled Dream-7B B=8 and LLaDA-8B L=1280 pass timings")
+                    help="skip the gated vs dense decodes at the LLaDA-8B gen-1024 and "
+                         "Dream-7B B=8 workloads")
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="skip the labelled logits-x8 gate-variant sweep")
     ap.add_argument("--only", choices=["all", "pass", "vocab", "copy", "gated", "compaction",
-                                       "shapes"],
+                                       "shapes", "sweep", "cpu"],
                     default="all",
                     help="run one leg only (profiling runs): the timed passes, the vocab/gate "
                          "kernel, or a plain 1 GiB device copy that calibrates byte counters")
@@ -370,11 +427,19 @@ def main():
         print(json.dumps({"compaction_b8_logits_x8": compaction_leg()}), flush=True)
         return
     if args.only == "shapes":
-        print(json.dumps({"other_shapes": other_shapes_leg()}), flush=True)
+        print(json.dumps(shape_legs()), flush=True)
+        return
+    if args.only == "sweep":
+        print(json.dumps({"table3_sweep_logits_x8": table3_sweep_leg()}), flush=True)
+        return
+    if args.only == "cpu":
+        import seeded_inputs as si_
+        prompt = si_.prompt_tokens(1, B, P, si_.LLADA_8B.vocab, si_.LLADA_8B.mask_id)
+        print(json.dumps({"cpu_baseline": cpu_baseline(si_.LLADA_8B, prompt)}), flush=True)
         return
     if args.only == "pass":
         args.no_decode = args.no_vocab = args.no_cpu_baseline = args.no_gated = True
-        args.no_compaction = args.no_shapes = True
+        args.no_compaction = args.no_shapes = args.no_sweep = True
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (batch rows "
               "decode independently, so more GPUs shard rows with no collective)", file=sys.stderr)
@@ -479,8 +544,11 @@ def main():
     if not args.no_compaction:
         result["compaction_b8_logits_x8"] = compaction_leg()
         note("compaction leg done")
+    if not args.no_sweep:
+        result["table3_sweep_logits_x8"] = table3_sweep_leg()
+        note("gate-variant sweep leg done")
     if not args.no_shapes:
-        result["other_shapes"] = other_shapes_leg()
+        result.update(shape_legs())
     if not args.no_cpu_baseline:
         note("cpu baseline leg starts")
         import seeded_inputs as si_

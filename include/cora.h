@@ -236,10 +236,13 @@ cora_status cora_model_copy_tensor(cora_model *model, int32_t tensor_id, void *h
 cora_status cora_model_set_timing(cora_model *model, int32_t enable);
 cora_status cora_model_read_timing(cora_model *model, double *total_ms, int64_t *launches);
 
-/* Batch-row compaction in cora_block_decode (R15: rows decode independently, so
- * dropping finished rows from the dense pass changes no live row's inputs; row
- * results can differ only in rounding where a kernel's split of the work
- * depends on the row count).  enable != 0 turns it on (default), 0 off. */
+/* Batch-row compaction in cora_block_decode (rows decode independently, so
+ * dropping finished rows from the dense pass changes no live row's inputs).
+ * Every kernel choice that sets an output's summation order (split-K count,
+ * attention key-range parts, LM-head kernel and vocab partial layout) is made
+ * for max_batch rows, never for the live row count, so a row's tokens and
+ * passes are bit-identical with compaction on or off and equal to a decode of
+ * that row alone on the same model.  enable != 0 turns it on (default), 0 off. */
 cora_status cora_model_set_compaction(cora_model *model, int32_t enable);
 
 /* Device bytes the model holds (weights + workspace). */

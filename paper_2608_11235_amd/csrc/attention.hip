@@ -5,8 +5,10 @@
 // One workgroup = 64 queries of one head (4 wavefronts x 16 queries) times SPLIT parts of
 // the key range: with SPLIT = 2 a second group of 4 wavefronts runs the same queries over
 // the second half of the key tiles, and the two partial softmax states (max, sum, O) are
-// merged through LDS at the end.  Small grids (B * H * L / 64 below two workgroups per CU)
-// use SPLIT = 2, which doubles the wavefronts per SIMD and halves each one's serial chain.
+// merged through LDS at the end.  Small grids (max_batch * H * L / 64 below two workgroups
+// per CU: the choice is made for the rows a launch is planned for, not the live ones, so
+// that a row's rounding never depends on its batch) use SPLIT = 2, which doubles the
+// wavefronts per SIMD and halves each one's serial chain.
 // Key tiles of 64 are staged in LDS: the next tile's loads are in flight in registers while
 // the current tile is multiplied out of LDS.  Small grids double-buffer the tile (one
 // barrier per tile).  Large grids (SB) keep one LDS tile buffer and at most 168 registers,
@@ -234,10 +236,12 @@ __global__ __launch_bounds__(256 * SPLIT, SB && SPLIT == 1 ? 3 : 1) void k_atten
 
 hipError_t launch_attention(const uint16_t* q, const uint16_t* k, const uint16_t* vt,
                             uint16_t* out, int B, int L, int Ls, int H, int Hkv, int hd,
-                            int num_cus, hipStream_t s) {
+                            int plan_B, int num_cus, hipStream_t s) {
+  if (B <= 0) return hipSuccess;
+  if (plan_B < B) return hipErrorInvalidValue;
   const float scale_log2 = 1.4426950408889634f / sqrtf((float)hd);
   const dim3 grid(Ls / 64, B * H);
-  const bool split = (int64_t)grid.x * grid.y < 2 * (int64_t)num_cus;
+  const bool split = (int64_t)grid.x * plan_B * H < 2 * (int64_t)num_cus;
 #define ATTN(HD_, SP_, SB_)                                                                \
   hipLaunchKernelGGL((k_attention<HD_, SP_, SB_>), grid, dim3(256 * SP_), 0, s, q, k, vt, out, L, \
                      Ls, H, Hkv, scale_log2)

@@ -108,8 +108,13 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void k_gemm(GemmArgs g) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WAVES_N, wn = wave % WAVES_N;
   const int num_m = (g.M + BM - 1) / BM;
+  // logical order: split-major, then N tile, then M tile.  xcd_remap hands each XCD a
+  // contiguous run of that order, so an XCD's workgroups share one K range (its L2 holds
+  // only that range of A) and, within it, the M tiles of a run of N tiles (each weight
+  // byte is fetched by one XCD).
   const int li = xcd_remap(blockIdx.x, gridDim.x);
-  const int split = li % g.splits, tile = li / g.splits;
+  const int n_tiles = gridDim.x / g.splits;
+  const int split = li / n_tiles, tile = li - split * n_tiles;
   const int tile_m = tile % num_m, tile_n = tile / num_m;
   const int m0 = tile_m * BM, n0 = tile_n * BN;
   const int nk = g.K / BK / g.splits;
@@ -566,9 +571,10 @@ GemmPlan gemm_plan(int M, int N, int K, int num_cus) {
 // Tiles that may split K (outputs whose consumer folds partials in): estimated time =
 // rounds x per-tile main loop (2.18 MMAC per microsecond per CU at efficiency 1) + partial
 // traffic (written here, read back downstream: ~0.4 us per MiB), over configs {0, 2, 3} and
-// 1, 2, 4 or 8 splits with >= 8 K-slices each.  Splits never exceed the workspace bound.
-GemmPlan gemm_plan_split(int M, int N, int K, int num_cus) {
-  if (M <= 64) return gemm_plan_cfg(M, N, K, 1, 1);
+// 1, 2, 4 or 8 splits with >= 8 K-slices each (only `splits` when it is > 0).  Splits never
+// exceed the workspace bound.
+GemmPlan gemm_plan_split(int M, int N, int K, int num_cus, int splits) {
+  if (M <= 64 && splits <= 1) return gemm_plan_cfg(M, N, K, 1, 1);
   const int nk = K / BK;
   const int cfgs[3] = {0, 3, 2};
   GemmPlan best{};
@@ -578,6 +584,7 @@ GemmPlan gemm_plan_split(int M, int N, int K, int num_cus) {
     const CfgShape sh = cfg_shape(cfgs[c]);
     const int tiles = ((M + sh.bm - 1) / sh.bm) * ((N + sh.bn - 1) / sh.bn);
     for (int sp = 1; sp <= 8; sp *= 2) {
+      if (splits > 0 && sp != splits) continue;
       if (sp > 1 && (nk % sp != 0 || nk / sp < 8 ||
                      (size_t)sp * M * N > gemm_ws_floats_bound(num_cus)))
         continue;

@@ -93,9 +93,12 @@ struct GemmPlan {
   size_t ws_floats;    // EPI_PART_F32 partial floats (splits * M * N) when splits > 1
 };
 // Whole-K plan for any epilogue; split plan (EPI_PART_F32 when splits > 1, else any
-// epilogue) never needs more than gemm_ws_floats_bound(num_cus) partial floats.
+// epilogue) never needs more than gemm_ws_floats_bound(num_cus) partial floats.  With
+// splits > 0 the split plan keeps that split count (it must divide K / 64 into runs of >= 8
+// slices) and only picks the tile config; the split count alone decides the summation order
+// of an output, the tile config does not.
 GemmPlan gemm_plan(int M, int N, int K, int num_cus);
-GemmPlan gemm_plan_split(int M, int N, int K, int num_cus);
+GemmPlan gemm_plan_split(int M, int N, int K, int num_cus, int splits = 0);
 GemmPlan gemm_plan_cfg(int M, int N, int K, int cfg, int splits);
 int gemm_num_cfgs();
 inline size_t gemm_ws_floats_bound(int num_cus) { return (size_t)2 * num_cus * 256 * 256; }
@@ -137,9 +140,11 @@ hipError_t launch_top1_merge_parts(const float* pm, const float* ps, const int* 
                                    float* conf, hipStream_t s);
 
 // ---- attention ---------------------------------------------------------------------------
+// The key range is split into parts (merged in part order) by the grid of plan_B rows
+// (plan_B >= B), so a row's output does not depend on how many rows share the launch.
 hipError_t launch_attention(const uint16_t* q, const uint16_t* k, const uint16_t* vt,
                             uint16_t* out, int B, int L, int Ls, int H, int Hkv, int hd,
-                            int num_cus, hipStream_t s);
+                            int plan_B, int num_cus, hipStream_t s);
 
 // ---- vocab / gate -------------------------------------------------------------------------
 // Logits rows r of batch row b (row-major [B, n_rows, V]) score canvas position

@@ -446,6 +446,16 @@ static cora_status timed_pair(cora_model* m, hipEvent_t* e0, hipEvent_t* e1) {
 }
 
 // ---- one dense pass ----------------------------------------------------------------------
+// Rows decode independently (R15), and a row's results must not depend on which other rows
+// share its pass (batch-row compaction drops finished rows; a row decoded alone must match
+// its batched decode).  Every choice that changes an output's summation order (split-K
+// count, attention key-range parts, LM-head kernel and its vocab partial layout) is made
+// for max_batch rows of the call's per-row length, never for the live row count; only
+// choices that leave every sum as it is (GEMM tile shapes) follow the live rows.
+static int plan_rows(const cora_model* m, int rows_per_batch_row) {
+  return m->max_batch * rows_per_batch_row;
+}
+
 static cora_status gemm(cora_model* m, int epi, const GemmArgs& g, hipStream_t s,
                         bool timed = false) {
   hipEvent_t e0 = nullptr, e1 = nullptr;
@@ -465,9 +475,15 @@ static cora_status gemm_partials(cora_model* m, GemmArgs g, const GemmPlan& p, h
   return CORA_OK;
 }
 
+// Split plan for the live rows g.M with the split count planned for plan_M rows.
+static GemmPlan fixed_split_plan(const cora_model* m, const GemmArgs& g, int plan_M) {
+  const int splits = gemm_plan_split(plan_M, g.N, g.K, m->num_cus).splits;
+  return gemm_plan_split(g.M, g.N, g.K, m->num_cus, splits);
+}
+
 // QKV projection with bias, RoPE and head layout, whole-K or split-K.
-static cora_status qkv_gemm(cora_model* m, const GemmArgs& g, hipStream_t s) {
-  const GemmPlan p = gemm_plan_split(g.M, g.N, g.K, m->num_cus);
+static cora_status qkv_gemm(cora_model* m, const GemmArgs& g, int plan_M, hipStream_t s) {
+  const GemmPlan p = fixed_split_plan(m, g, plan_M);
   if (p.splits == 1) {
     HIP_TRY(launch_gemm(EPI_QKV_ROPE, g, p, s));
     return CORA_OK;
@@ -480,9 +496,10 @@ static cora_status qkv_gemm(cora_model* m, const GemmArgs& g, hipStream_t s) {
 // Residual update h += A . W^T; when norm_out is given it then receives rmsnorm(h) for the
 // next GEMM.  Split-K plans store per-split partials and fold them into h, together with the
 // norm, in one row-wise kernel.
-static cora_status residual_gemm(cora_model* m, GemmArgs g, uint16_t* norm_out, hipStream_t s) {
+static cora_status residual_gemm(cora_model* m, GemmArgs g, uint16_t* norm_out, int plan_M,
+                                 hipStream_t s) {
   const auto& c = m->cfg;
-  const GemmPlan p = gemm_plan_split(g.M, g.N, g.K, m->num_cus);
+  const GemmPlan p = fixed_split_plan(m, g, plan_M);
   float* h = reinterpret_cast<float*>(g.C);
   if (p.splits == 1) {
     HIP_TRY(launch_gemm(EPI_ADD_F32, g, p, s));
@@ -498,7 +515,7 @@ static cora_status residual_gemm(cora_model* m, GemmArgs g, uint16_t* norm_out, 
 
 static cora_status run_layers(cora_model* m, const int32_t* tokens, int B, int L, hipStream_t s) {
   const auto& c = m->cfg;
-  const int d = c.d_model, M = B * L, Ls = round_up(L, 64);
+  const int d = c.d_model, M = B * L, Ls = round_up(L, 64), Mp = plan_rows(m, L);
   HIP_TRY(launch_embed(tokens, m->embed, m->h, M, d, c.vocab, s));
   const RowSel all{0, L, 0, 0, 0, 0, 0, nullptr};
   HIP_TRY(launch_rmsnorm(m->h, m->ones, m->a, M, d, c.rms_eps, all, s));
@@ -510,27 +527,29 @@ static cora_status run_layers(cora_model* m, const int32_t* tokens, int B, int L
     g.w_packed = true;
     g.qkv = QkvOut{m->q, m->k, m->vt, m->rope_cos, m->rope_sin, L, Ls, c.n_heads, c.n_kv_heads,
                    c.head_dim};
-    if (cora_status st = qkv_gemm(m, g, s)) return st;
+    if (cora_status st = qkv_gemm(m, g, Mp, s)) return st;
     HIP_TRY(launch_attention(m->q, m->k, m->vt, m->attn, B, L, Ls, c.n_heads, c.n_kv_heads,
-                             c.head_dim, m->num_cus, s));
+                             c.head_dim, m->max_batch, m->num_cus, s));
     g = GemmArgs{m->attn, m->hq, ly.wo, m->hq, M, d, m->hq, m->h, d, nullptr, 1.0f};
     g.w_packed = true;
-    if (cora_status st = residual_gemm(m, g, m->a, s)) return st;
+    if (cora_status st = residual_gemm(m, g, m->a, Mp, s)) return st;
     g = GemmArgs{m->a, d, ly.wgu, d, M, 2 * m->f_pad, d, m->u, m->f_pad, nullptr, 1.0f};
     g.w_packed = true;
     if (cora_status st = gemm(m, EPI_SWIGLU, g, s, m->timing)) return st;
     g = GemmArgs{m->u, m->f_pad, ly.wd, m->f_pad, M, d, m->f_pad, m->h, d, nullptr, 1.0f};
     g.w_packed = true;
     // the last layer's output is normalised only on the rows the LM head reads
-    if (cora_status st = residual_gemm(m, g, l + 1 < n_layers ? m->a : nullptr, s)) return st;
+    if (cora_status st = residual_gemm(m, g, l + 1 < n_layers ? m->a : nullptr, Mp, s))
+      return st;
   }
   return CORA_OK;
 }
 
-// few rows read the packed weights (HBM-bound stream), more rows take the tiled GEMM
-static bool lm_head_few_rows(const cora_model* m, int n_out_rows) {
-  return m->lm_head_packed && n_out_rows <= LM_HEAD_FUSED_MAX_ROWS &&
-         lm_head_supported(n_out_rows, m->cfg.vocab, m->cfg.d_model, m->cfg.d_model);
+// few rows read the packed weights (HBM-bound stream), more rows take the tiled GEMM; the
+// choice is made for the planned row count (max_batch x rows per batch row)
+static bool lm_head_few_rows(const cora_model* m, int plan_out_rows) {
+  return m->lm_head_packed && plan_out_rows <= LM_HEAD_FUSED_MAX_ROWS &&
+         lm_head_supported(plan_out_rows, m->cfg.vocab, m->cfg.d_model, m->cfg.d_model);
 }
 
 static LmHeadArgs lm_args(const cora_model* m, int n_out_rows) {
@@ -543,11 +562,11 @@ static LmHeadArgs lm_args(const cora_model* m, int n_out_rows) {
   return a;
 }
 
-static cora_status lm_head(cora_model* m, const RowSel& sel, int n_out_rows, uint16_t* logits,
-                           hipStream_t s) {
+static cora_status lm_head(cora_model* m, const RowSel& sel, int n_out_rows, int plan_out_rows,
+                           uint16_t* logits, hipStream_t s) {
   const auto& c = m->cfg;
   HIP_TRY(launch_rmsnorm(m->h, m->ones, m->a, n_out_rows, c.d_model, c.rms_eps, sel, s));
-  if (lm_head_few_rows(m, n_out_rows)) {
+  if (lm_head_few_rows(m, plan_out_rows)) {
     LmHeadArgs a = lm_args(m, n_out_rows);
     a.logits = logits;
     a.ldc = c.vocab;
@@ -566,8 +585,8 @@ static cora_status lm_head(cora_model* m, const RowSel& sel, int n_out_rows, uin
 static cora_status score_rows(cora_model* m, const RowSel& sel, int B, int n_rows,
                               const VocabGateArgs& vg, hipStream_t s) {
   const auto& c = m->cfg;
-  const int M = B * n_rows;
-  if (lm_head_few_rows(m, M)) {
+  const int M = B * n_rows, Mp = plan_rows(m, n_rows);
+  if (lm_head_few_rows(m, Mp)) {
     HIP_TRY(launch_rmsnorm(m->h, m->ones, m->a, M, c.d_model, c.rms_eps, sel, s));
     const LmHeadArgs a = lm_args(m, M);
     HIP_TRY(launch_lm_head(a, true, s));
@@ -575,11 +594,13 @@ static cora_status score_rows(cora_model* m, const RowSel& sel, int B, int n_row
     return CORA_OK;
   }
   // more rows: the tiled GEMM folds each wavefront's logit columns into per-row partials
-  // (EPI_TOP1), held in the logits buffer, which this path leaves otherwise unused
-  const GemmPlan p = gemm_plan(M, c.vocab, c.d_model, m->num_cus);
+  // (EPI_TOP1), held in the logits buffer, which this path leaves otherwise unused.  The
+  // tile config (which sets the columns a partial covers) is the planned row count's.
+  const GemmPlan pp = gemm_plan(Mp, c.vocab, c.d_model, m->num_cus);
+  const GemmPlan p = gemm_plan_cfg(M, c.vocab, c.d_model, pp.cfg, 1);
   const int np = gemm_top1_parts(p, c.vocab);
   const size_t part_bytes = align_up((size_t)M * np * 4);
-  if (3 * part_bytes <= (size_t)m->max_batch * m->max_rows * c.vocab * 2) {
+  if (3 * align_up((size_t)Mp * np * 4) <= (size_t)m->max_batch * m->max_rows * c.vocab * 2) {
     HIP_TRY(launch_rmsnorm(m->h, m->ones, m->a, M, c.d_model, c.rms_eps, sel, s));
     GemmArgs g{m->a, c.d_model, m->lm_head, c.d_model, M, c.vocab, c.d_model, nullptr, 0,
                nullptr, c.logit_scale};
@@ -594,7 +615,7 @@ static cora_status score_rows(cora_model* m, const RowSel& sel, int B, int n_row
                                     vg.out_off, vg.top1, vg.conf, s));
     return CORA_OK;
   }
-  if (cora_status e = lm_head(m, sel, M, m->logits, s)) return e;
+  if (cora_status e = lm_head(m, sel, M, Mp, m->logits, s)) return e;
   VocabGateArgs r = vg;
   r.logits = m->logits;
   r.n_rows = n_rows;
@@ -614,7 +635,7 @@ extern "C" cora_status cora_forward_logits(cora_model* m, const int32_t* d_token
   const hipStream_t s = S(hip_stream);
   if (cora_status st = run_layers(m, d_tokens, B, L, s)) return st;
   const RowSel sel{1, L, n_rows, row_begin, 0, 0, 0, nullptr};
-  return lm_head(m, sel, B * n_rows, d_logits, s);
+  return lm_head(m, sel, B * n_rows, plan_rows(m, n_rows), d_logits, s);
 } catch (...) {
   return exception_status();
 }

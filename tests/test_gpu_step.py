@@ -19,7 +19,8 @@ import seeded_inputs as si
 from oracle import decode
 from oracle import forward as of
 from tests.gpu_common import log_case, require_gpu, to_dev
-from tests.parity import CONF_RTOL, bf16_to_f32, logit_tolerance, margins
+from tests.parity import (CONF_RTOL, bf16_to_f32, comparable_decisions, describe_error,
+                          logit_tolerance, margins)
 
 pytestmark = pytest.mark.gpu
 
@@ -29,6 +30,10 @@ SPEC = si.TINY
 # within the bf16 logit error and excluded.  The same shape drawn with std 0.07 (logits x2)
 # spreads confidences and margins while bf16 activation rounding stays under 1.4 % of the
 # largest logit, so over half of the decisions are comparable; it is an extra parity model.
+# On the tiny model itself only a few decisions per decode clear the bf16 error (3/488 and
+# 4/544 measured), so there the test requires a nonzero count; the step's decision logic at
+# that config is compared on nearly every position against the oracle run on the GPU's own
+# logits (tests/test_gpu_own_logits.py).
 SEPARATED = replace(si.TINY, name="tiny-std0.07", init_std=0.07, logit_scale=2.0)
 MODELS = [pytest.param(SPEC, 0.0, id="tiny"), pytest.param(SEPARATED, 0.4, id="tiny-std0.07")]
 P, G, BLK, S = 32, 64, 32, 16
@@ -44,32 +49,10 @@ def _logits_fn(spec=SPEC):
 
 
 def _comparable(o, pre_unres, lo, D, delta_p, gate_on, blk=BLK):
-    """Per block position: can a logit error of D (per row) flip its decision?
-    ln c moves by at most 2 D, so each candidate's ln c lies in [ln c - 2D, ln c + 2D].
-    A candidate is certainly fixed by the transfer rule if fewer than k others could rank
-    above it, certainly not if at least k others certainly rank above it (P3); a residual
-    candidate's gate outcome is certain if ln c is farther than 2D from ln delta_p and its
-    top-1 (hence its counter) is certain (P2, P1).  Returns (decision_ok, top1_ok)."""
-    c = np.asarray(o["c"], np.float64)
-    lnc = np.log(c)
-    p1 = o["gamma"] > 2 * D                                          # P1
+    """Decision and top-1 comparability of the block positions (P1-P3, tests/parity.py)."""
     U = pre_unres[lo:lo + blk] == 1
-    idx = np.where(U)[0]
-    k = o["k"]
-    r = np.maximum(2 * D, CONF_RTOL)
-    hi, lo_ = lnc + r, lnc - r
-    T = set((np.asarray(o["T"]) - lo).tolist())
-    dec_ok = np.ones(blk, bool)
-    for i in idx:
-        others = idx[idx != i]
-        maybe_above = int(np.sum(hi[others] >= lo_[i]))
-        surely_above = int(np.sum(lo_[others] > hi[i]))
-        in_T_sure, out_T_sure = maybe_above < k, surely_above >= k
-        ok = in_T_sure or out_T_sure                                  # P3
-        if ok and gate_on and i not in T:                             # P2 (+ P1 for m)
-            ok = abs(lnc[i] - np.log(delta_p)) > r[i] and bool(p1[i])
-        dec_ok[i] = ok
-    return dec_ok, p1
+    return comparable_decisions(o["c"], o["gamma"], np.asarray(o["T"]) - lo, o["k"], U, D,
+                                delta_p, gate_on)
 
 
 @pytest.mark.parametrize("spec,min_frac", MODELS)
@@ -82,7 +65,7 @@ def test_teacher_forced_steps(delta_p, m_req, gate_on, spec, min_frac):
     _, _, trace = decode.block_decode(_logits_fn(spec), prompt, G, spec.mask_id, BLK, S, delta_p,
                                       m_req, gate_on, record=True)
     n_dec = n_dec_ok = 0
-    worst = 0.0
+    worst, worst_desc = 0.0, ""
     with Model(spec, seed=0, max_batch=1, max_seq=L) as m:
         for si_, step in enumerate(trace):
             log_case(f"teacher-forced {spec.name} step {si_} dp={delta_p} m={m_req} gate={gate_on}")
@@ -92,8 +75,9 @@ def test_teacher_forced_steps(delta_p, m_req, gate_on, spec, min_frac):
                              .cpu().numpy())[0].astype(np.float64)
             ref = step["logits"][0]
             D = np.max(np.abs(lg - ref), axis=-1)
-            worst = max(worst, D.max() / np.max(np.abs(ref)))
-            assert D.max() <= logit_tolerance(ref), f"step {si_}: logit error {D.max()}"
+            if D.max() / np.max(np.abs(ref)) > worst:
+                worst, worst_desc = D.max() / np.max(np.abs(ref)), describe_error(D.max(), ref)
+            assert D.max() <= logit_tolerance(ref), f"step {si_}: {describe_error(D.max(), ref)}"
             st = DecodeState.from_host(pre, P, G, BLK, BLK)
             m.denoise_step(st, Sched(BLK, S), Gate(delta_p, m_req, gate_on))
             gpu = st.to_host()
@@ -128,8 +112,8 @@ def test_teacher_forced_steps(delta_p, m_req, gate_on, spec, min_frac):
                 for n in ("block_idx", "step_idx"):
                     assert (gpu[n] == nxt[n]).all(), f"step {si_} {n}"
     print(f"[summary] steps {len(trace)}: unresolved-position decisions compared "
-          f"{n_dec_ok}/{n_dec}, worst max|dl|/max|l| = {worst:.4f}")
-    assert n_dec_ok >= min_frac * n_dec
+          f"{n_dec_ok}/{n_dec}, worst step: {worst_desc}")
+    assert n_dec_ok >= max(min_frac * n_dec, 1)
 
 
 @pytest.mark.parametrize("spec,min_frac", MODELS)
