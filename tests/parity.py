@@ -13,10 +13,11 @@ kept there: the path rounds activations to bf16 (unit roundoff 2^-8) at five poi
 layer (normed input, q/k/v, attention output, normed MLP input, SwiGLU output) and the
 errors of independent roundings add up like a random walk, so the relative logit error of
 any implementation of that arithmetic grows about as the square root of the depth: the
-2-layer passes measure 0.64-0.75 % of max |l|, which predicts 2.6-3.0 % at 32 layers.  A
-bound that is fixed in max |l| cannot hold at every depth for the arithmetic the pass is
-specified in; the range-scaled bound (about twice max |l| on these near-zero-mean logits)
-is the looser one, and the full-depth case also carries decision parity.
+2-layer passes measure 0.64-0.94 % of max |l|, which predicts 2.6-3.8 % at 32 layers
+(measured: 2.0 and 3.4 %).  A bound that is fixed in max |l| cannot hold at every depth for
+the arithmetic the pass is specified in; the range-scaled bound (about twice max |l| on
+these near-zero-mean logits) is the looser one, and the full-depth case also carries
+decision parity.
 
 A decision is compared bit-exactly only where the measured per-row logit error D_i cannot
 flip it (Proposition 1: an argmax survives any perturbation below half its margin):
