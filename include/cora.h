@@ -205,6 +205,29 @@ cora_status cora_vocab_gate(const uint16_t *d_logits, int32_t n_rows, int32_t ro
                             const cora_sched_cfg *sched, const cora_gate_cfg *gate,
                             void *hip_stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation): cora_vocab_gate with
+ * the same arguments, outputs and error behaviour, computed without any
+ * allocation.  Each logits row's vocabulary is split into consecutive ranges,
+ * one workgroup each (so few rows still fill the GPU); their partial (max,
+ * sum of exp, lowest arg max) go to a fixed device array of the library of
+ * CORA_VOCAB_GATE_NOALLOC_MAX_PARTIALS entries (12 bytes each, 3 MiB per GPU,
+ * held until the process ends) and are merged in vocab order.  top1 equals
+ * cora_vocab_gate's bit for bit; conf differs only in fp32 summation order,
+ * so decisions agree except where a cut or threshold lies within that
+ * rounding.  B * n_rows above CORA_VOCAB_GATE_NOALLOC_MAX_PARTIALS returns
+ * CORA_ERR_UNSUPPORTED.  The array's address is looked up on the first call
+ * on a device (the current device, which must own the stream and pointers).
+ * Every call on one GPU shares that array: calls that overlap on one GPU
+ * (other threads, other streams) race and must be ordered by the caller.
+ * No hipMalloc, hipFree or other allocating routine is called, also not on
+ * error paths.  Asynchronous. */
+#define CORA_VOCAB_GATE_NOALLOC_MAX_PARTIALS 262144
+cora_status cora_vocab_gate_noalloc(const uint16_t *d_logits, int32_t n_rows, int32_t row_begin,
+                                    int32_t V, int32_t mask_id, cora_state *state,
+                                    int32_t k_transfer, const cora_sched_cfg *sched,
+                                    const cora_gate_cfg *gate, void *hip_stream);
+
 /* Gated block decode of B prompts (d_prompt int32 [B, prompt_len], device):
  * the canvas starts as prompt + gen_len masks, rows decode independently and
  * each block ends once it holds no unresolved position, skipping its

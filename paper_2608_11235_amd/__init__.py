@@ -11,7 +11,7 @@ supplies device memory and the HIP stream only.
     vocab_gate(logits, ...)                 the vocab/gate kernel alone
 """
 from .api import (  # noqa: F401
-    Model, DecodeState, Sched, Gate, vocab_gate, model_cfg_from,
+    Model, DecodeState, Sched, Gate, vocab_gate, vocab_gate_noalloc, model_cfg_from,
     TENSOR_EMBED, TENSOR_LM_HEAD, layer_tensor_id,
 )
 from .configs import TINY, LLADA_8B, DREAM_7B, ModelConfig  # noqa: F401

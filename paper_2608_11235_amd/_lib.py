@@ -49,6 +49,9 @@ EXPORTS = {
                                   ctypes.POINTER(GateCfg), c_vp]),
     "cora_vocab_gate": (c_i32, [c_vp, c_i32, c_i32, c_i32, c_i32, ctypes.POINTER(State), c_i32,
                                 ctypes.POINTER(SchedCfg), ctypes.POINTER(GateCfg), c_vp]),
+    "cora_vocab_gate_noalloc": (c_i32, [c_vp, c_i32, c_i32, c_i32, c_i32, ctypes.POINTER(State),
+                                        c_i32, ctypes.POINTER(SchedCfg), ctypes.POINTER(GateCfg),
+                                        c_vp]),
     "cora_block_decode": (c_i32, [c_vp, c_vp, c_i32, c_i32, c_i32, ctypes.POINTER(SchedCfg),
                                   ctypes.POINTER(GateCfg), c_vp, c_vp, c_vp, c_vp]),
     "cora_model_copy_tensor": (c_i32, [c_vp, c_i32, c_vp, c_sz]),

@@ -230,3 +230,14 @@ def vocab_gate(logits, n_rows, row_begin, V, mask_id, state: DecodeState, k_tran
                                        ctypes.byref(st), k_transfer, ctypes.byref(sc),
                                        ctypes.byref(gt), stream_handle(stream)),
           "cora_vocab_gate")
+
+
+def vocab_gate_noalloc(logits, n_rows, row_begin, V, mask_id, state: DecodeState, k_transfer,
+                       sched: Sched, gate: Gate, stream=None):
+    """cora_vocab_gate_noalloc: vocab_gate without any allocation (split rows, fixed scratch)."""
+    check_device_tensor(logits, "logits", _BF16_BITS, state.B * n_rows * V)
+    st, sc, gt = state.c(), sched.c(), gate.c()
+    check(_lib.load().cora_vocab_gate_noalloc(ptr(logits), n_rows, row_begin, V, mask_id,
+                                               ctypes.byref(st), k_transfer, ctypes.byref(sc),
+                                               ctypes.byref(gt), stream_handle(stream)),
+          "cora_vocab_gate_noalloc")

@@ -165,6 +165,18 @@ struct VocabGateArgs {
 };
 // top-1 and confidence of every logits row
 hipError_t launch_vocab_top1(const VocabGateArgs& a, hipStream_t s);
+// The same with each row's vocabulary split into `parts` consecutive ranges, one workgroup
+// each, whose (max, sum, lowest arg max) partials go to pm / ps / pa [rows * parts] (caller
+// memory, fully overwritten) and are folded in vocab order by k_top1_merge.  top1 agrees
+// with launch_vocab_top1 bit for bit; conf differs only in the fp32 summation order.
+struct VocabSplit {
+  int parts, chunks;  // chunks: set by the launcher (16-byte chunks, or entries, per part)
+  float* pm; float* ps; int* pa;
+};
+// parts for `rows` rows: ~4 workgroups per CU, each part >= 1024 chunks, rows * parts <=
+// max_partials; 0 when even one part per row does not fit
+int vocab_split_parts(int rows, int V, int num_cus, int64_t max_partials);
+hipError_t launch_vocab_top1_split(const VocabGateArgs& a, const VocabSplit& sp, hipStream_t s);
 // decision rules per batch row, reading the scores of rows [row_begin, row_begin + n_rows)
 // (n_rows == out_ld) or of the active block (row_begin < 0)
 hipError_t launch_gate_rules(const VocabGateArgs& a, hipStream_t s);

@@ -1,7 +1,10 @@
 // Host runtime behind the C ABI: model and workspace ownership, the launch
 // sequence of one dense pass, the denoising step, and the gated block decode loop.
 #include <math.h>
+#include <stdio.h>
 #include <string.h>
+
+#include <mutex>
 
 #include <string>
 #include <algorithm>
@@ -17,16 +20,15 @@ using namespace cora;
 
 namespace {
 
-thread_local std::string g_err;
+// last error message of this thread: a fixed buffer, so reporting an error allocates nothing
+thread_local char g_err[512];
 
-cora_status fail(cora_status st, const std::string& msg) noexcept {
-  try {
-    g_err = msg;
-  } catch (...) {
-    g_err.clear();
-  }
+cora_status fail(cora_status st, const char* msg) noexcept {
+  snprintf(g_err, sizeof(g_err), "%s", msg ? msg : "");
   return st;
 }
+
+cora_status fail(cora_status st, const std::string& msg) noexcept { return fail(st, msg.c_str()); }
 
 // An exception escaping an entry point becomes a status (the C ABI never throws): host
 // allocation failure is CORA_ERR_OOM, anything else CORA_ERR_UNSUPPORTED with its text.
@@ -157,7 +159,7 @@ static cora_status validate_cfg(const cora_model_cfg& c) {
 static hipStream_t S(void* s) { return reinterpret_cast<hipStream_t>(s); }
 
 // ---------------------------------------------------------------------------------------
-extern "C" const char* cora_last_error(void) { return g_err.c_str(); }
+extern "C" const char* cora_last_error(void) { return g_err; }
 
 extern "C" cora_status cora_model_destroy(cora_model* m) try {
   if (!m) return CORA_OK;
@@ -687,10 +689,9 @@ static VocabGateArgs vg_args(const uint16_t* logits, int n_rows, int row_begin, 
   return a;
 }
 
-extern "C" cora_status cora_vocab_gate(const uint16_t* d_logits, int32_t n_rows, int32_t row_begin,
-                                       int32_t V, int32_t mask_id, cora_state* st,
-                                       int32_t k_transfer, const cora_sched_cfg* sc,
-                                       const cora_gate_cfg* gt, void* hip_stream) try {
+static cora_status check_vocab_gate(const uint16_t* d_logits, int32_t n_rows, int32_t row_begin,
+                                    int32_t V, int32_t mask_id, const cora_state* st,
+                                    const cora_sched_cfg* sc, const cora_gate_cfg* gt) {
   if (cora_status e = check_sched_gate(sc, gt)) return e;
   if (cora_status e = check_state(st, sc)) return e;
   if (!d_logits) return fail(CORA_ERR_INVALID_ARG, "null logits");
@@ -709,9 +710,88 @@ extern "C" cora_status cora_vocab_gate(const uint16_t* d_logits, int32_t n_rows,
                                       "the generation region");
   }
   if (n_rows <= 0) return fail(CORA_ERR_INVALID_ARG, "n_rows must be positive");
+  return CORA_OK;
+}
+
+extern "C" cora_status cora_vocab_gate(const uint16_t* d_logits, int32_t n_rows, int32_t row_begin,
+                                       int32_t V, int32_t mask_id, cora_state* st,
+                                       int32_t k_transfer, const cora_sched_cfg* sc,
+                                       const cora_gate_cfg* gt, void* hip_stream) try {
+  if (cora_status e = check_vocab_gate(d_logits, n_rows, row_begin, V, mask_id, st, sc, gt))
+    return e;
   const VocabGateArgs a = vg_args(d_logits, n_rows, row_begin, V, mask_id, st, k_transfer, sc, gt);
   HIP_TRY(launch_vocab_top1(a, S(hip_stream)));
   HIP_TRY(launch_gate_rules(a, S(hip_stream)));
+  return CORA_OK;
+} catch (...) {
+  return exception_status();
+}
+
+// ---- the vocab/gate kernels with a fixed scratch array --------------------------------------
+// Partials of the split row reduction live in `scratch`, a file-scope device array (one copy
+// per GPU, held until the process ends).  In host code the array's name is only a host-side
+// stand-in: its device address is looked up once per device with hipGetSymbolAddress, with
+// that device current, and only that address is handed to kernels.  Every call on one GPU
+// shares the array and overwrites the partials it reads (nothing must start at zero), so
+// calls that overlap on one GPU race.
+constexpr int64_t NOALLOC_PARTIALS = CORA_VOCAB_GATE_NOALLOC_MAX_PARTIALS;
+constexpr int MAX_DEVICES = 64;
+static __device__ __align__(256) unsigned char scratch[NOALLOC_PARTIALS * 12];
+static std::mutex g_scratch_mu;
+static void* g_scratch_ptr[MAX_DEVICES];
+static int g_scratch_cus[MAX_DEVICES];
+
+#define HIP_TRY_NOALLOC(expr)                                                        \
+  do {                                                                               \
+    hipError_t e_ = (expr);                                                          \
+    if (e_ != hipSuccess) {                                                          \
+      (void)hipGetLastError();                                                       \
+      snprintf(g_err, sizeof(g_err), "%s: %s", #expr, hipGetErrorString(e_));        \
+      return CORA_ERR_HIP;                                                           \
+    }                                                                                \
+  } while (0)
+
+static cora_status scratch_of_current_device(void** ptr, int* num_cus) {
+  int dev = 0;
+  HIP_TRY_NOALLOC(hipGetDevice(&dev));
+  if (dev < 0 || dev >= MAX_DEVICES) return fail(CORA_ERR_UNSUPPORTED, "device index >= 64");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    HIP_TRY_NOALLOC(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) return fail(CORA_ERR_HIP, "hipGetSymbolAddress returned a null scratch address");
+    int cus = 0;
+    HIP_TRY_NOALLOC(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+    g_scratch_cus[dev] = cus > 0 ? cus : 256;
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  *num_cus = g_scratch_cus[dev];
+  return CORA_OK;
+}
+
+extern "C" cora_status cora_vocab_gate_noalloc(const uint16_t* d_logits, int32_t n_rows,
+                                               int32_t row_begin, int32_t V, int32_t mask_id,
+                                               cora_state* st, int32_t k_transfer,
+                                               const cora_sched_cfg* sc, const cora_gate_cfg* gt,
+                                               void* hip_stream) try {
+  if (cora_status e = check_vocab_gate(d_logits, n_rows, row_begin, V, mask_id, st, sc, gt))
+    return e;
+  const int64_t rows = (int64_t)st->B * n_rows;
+  if (rows > NOALLOC_PARTIALS)
+    return fail(CORA_ERR_UNSUPPORTED, "B * n_rows exceeds the fixed scratch of "
+                                      "cora_vocab_gate_noalloc (262144 rows)");
+  void* base = nullptr;
+  int cus = 0;
+  if (cora_status e = scratch_of_current_device(&base, &cus)) return e;
+  const VocabGateArgs a = vg_args(d_logits, n_rows, row_begin, V, mask_id, st, k_transfer, sc, gt);
+  VocabSplit sp{};
+  sp.parts = vocab_split_parts((int)rows, V, cus, NOALLOC_PARTIALS);
+  sp.pm = reinterpret_cast<float*>(base);
+  sp.ps = sp.pm + NOALLOC_PARTIALS;
+  sp.pa = reinterpret_cast<int*>(sp.ps + NOALLOC_PARTIALS);
+  HIP_TRY_NOALLOC(launch_vocab_top1_split(a, sp, S(hip_stream)));
+  HIP_TRY_NOALLOC(launch_gate_rules(a, S(hip_stream)));
   return CORA_OK;
 } catch (...) {
   return exception_status();

@@ -26,6 +26,8 @@
 // completion, a ticket round trip) from every workgroup of the bandwidth-bound first pass.
 #include <limits.h>
 
+#include <algorithm>
+
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -71,9 +73,14 @@ __device__ __forceinline__ void consume32(TopState& t, BestChunk& best, const fl
   t.s += acc0 + acc1;
 }
 
-template <bool VEC>
-__global__ __launch_bounds__(256) void k_vocab_top1(VocabGateArgs a) {
-  const int row = blockIdx.x;
+// PART: workgroup blockIdx.x = row * sp.parts + part reduces vocab chunks [part * sp.chunks,
+// (part + 1) * sp.chunks) of its row (entries, not chunks, when !VEC) and stores the partial
+// (max, sum, lowest arg max) at sp.p*[blockIdx.x]; k_top1_merge folds a row's parts in vocab
+// order.  Without PART one workgroup covers the whole row and writes top1 / conf.
+template <bool VEC, bool PART>
+__global__ __launch_bounds__(256) void k_vocab_top1(VocabGateArgs a, VocabSplit sp) {
+  const int row = PART ? blockIdx.x / sp.parts : blockIdx.x;
+  const int part = PART ? blockIdx.x - row * sp.parts : 0;
   const int b = row / a.n_rows;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const uint16_t* x = a.logits + (int64_t)row * a.V;
@@ -84,7 +91,8 @@ __global__ __launch_bounds__(256) void k_vocab_top1(VocabGateArgs a) {
     // c, c + 256, c + 512, c + 768.  The next group's loads are in flight while the current
     // group is consumed.  Only a wavefront whose group holds the mask id's chunk (a scalar
     // test) applies the mask override.
-    const int nch = a.V >> 3;
+    const int c_lo = PART ? part * sp.chunks : 0;
+    const int nch = PART ? min(c_lo + sp.chunks, a.V >> 3) : a.V >> 3;  // end of this range
     const int mchunk = a.mask_id >> 3, mlane = a.mask_id & 7;
     const u32x4_t* xv = reinterpret_cast<const u32x4_t*>(x);
     const u32x4_t NEG_INF4 = {0xff80ff80u, 0xff80ff80u, 0xff80ff80u, 0xff80ff80u};
@@ -113,7 +121,7 @@ __global__ __launch_bounds__(256) void k_vocab_top1(VocabGateArgs a) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) w[i] = __builtin_nontemporal_load(xv + c + 256 * i);
     };
-    int c = tid;
+    int c = c_lo + tid;
     if (c + 768 < nch) {
       // two register groups used alternately (no copies): one in flight, one consumed
       u32x4_t ga[4], gb[4];
@@ -150,7 +158,9 @@ __global__ __launch_bounds__(256) void k_vocab_top1(VocabGateArgs a) {
       t.arg = found;
     }
   } else {
-    for (int v = tid; v < a.V; v += 256) {
+    const int v_lo = PART ? part * sp.chunks : 0;
+    const int v_hi = PART ? min(v_lo + sp.chunks, a.V) : a.V;
+    for (int v = v_lo + tid; v < v_hi; v += 256) {
       if (v == a.mask_id) continue;
       const float f = bf16_bits_to_f32(x[v]);
       if (f == -INFINITY) continue;
@@ -177,9 +187,15 @@ __global__ __launch_bounds__(256) void k_vocab_top1(VocabGateArgs a) {
   if (tid == 0) {
     TopState r{sm_m[0], sm_s[0], sm_a[0]};
     for (int w = 1; w < 4; ++w) r = merge(r, TopState{sm_m[w], sm_s[w], sm_a[w]});
-    const int64_t o = (int64_t)b * a.out_ld + a.out_off + (row - b * a.n_rows);
-    a.top1[o] = r.arg;
-    a.conf[o] = 1.0f / r.s;
+    if constexpr (PART) {
+      sp.pm[blockIdx.x] = r.m;
+      sp.ps[blockIdx.x] = r.s;
+      sp.pa[blockIdx.x] = r.arg;
+    } else {
+      const int64_t o = (int64_t)b * a.out_ld + a.out_off + (row - b * a.n_rows);
+      a.top1[o] = r.arg;
+      a.conf[o] = 1.0f / r.s;
+    }
   }
 }
 
@@ -296,11 +312,41 @@ __global__ __launch_bounds__(256) void k_gate_rules(VocabGateArgs a) {
 hipError_t launch_vocab_top1(const VocabGateArgs& a, hipStream_t s) {
   const int rows = a.B * a.n_rows;
   if (rows == 0) return hipSuccess;
+  const VocabSplit none{};
   if (a.V % 8 == 0)
-    hipLaunchKernelGGL(k_vocab_top1<true>, dim3(rows), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((k_vocab_top1<true, false>), dim3(rows), dim3(256), 0, s, a, none);
   else
-    hipLaunchKernelGGL(k_vocab_top1<false>, dim3(rows), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((k_vocab_top1<false, false>), dim3(rows), dim3(256), 0, s, a, none);
   return hipGetLastError();
+}
+
+int vocab_split_parts(int rows, int V, int num_cus, int64_t max_partials) {
+  if (rows <= 0 || (int64_t)rows > max_partials) return 0;
+  // each part keeps the 4-chunk load pipeline of every thread busy (>= 1024 chunks, or
+  // 8192 entries without 16-byte chunks); enough parts for ~4 workgroups per CU
+  const int units = V % 8 == 0 ? V / 8 : V;
+  const int min_units = V % 8 == 0 ? 1024 : 8192;
+  int parts = (4 * num_cus + rows - 1) / rows;
+  parts = std::min(parts, std::max(1, units / min_units));
+  parts = (int)std::min<int64_t>(parts, max_partials / rows);
+  return std::max(parts, 1);
+}
+
+hipError_t launch_vocab_top1_split(const VocabGateArgs& a, const VocabSplit& in, hipStream_t s) {
+  const int rows = a.B * a.n_rows;
+  if (rows == 0) return hipSuccess;
+  if (in.parts < 1 || !in.pm || !in.ps || !in.pa) return hipErrorInvalidValue;
+  VocabSplit sp = in;
+  const int units = a.V % 8 == 0 ? a.V / 8 : a.V;
+  sp.chunks = (units + sp.parts - 1) / sp.parts;
+  const dim3 grid((unsigned)((int64_t)rows * sp.parts));
+  if (a.V % 8 == 0)
+    hipLaunchKernelGGL((k_vocab_top1<true, true>), grid, dim3(256), 0, s, a, sp);
+  else
+    hipLaunchKernelGGL((k_vocab_top1<false, true>), grid, dim3(256), 0, s, a, sp);
+  if (hipError_t e = hipGetLastError()) return e;
+  return launch_top1_merge_parts(sp.pm, sp.ps, sp.pa, sp.parts, rows, a.n_rows, a.out_ld,
+                                 a.out_off, a.top1, a.conf, s);
 }
 
 hipError_t launch_gate_rules(const VocabGateArgs& a, hipStream_t s) {
