@@ -15,8 +15,12 @@
 // so three workgroups share a CU (three wavefronts per SIMD instead of two): each
 // wavefront's per-tile chain (MFMAs, max, lane exchange, exp, MFMAs) is latency-bound, and
 // the third wavefront hides more of it than the second barrier per tile costs.
-// Softmax terms use the hardware v_exp_f32 (arguments <= 0; results below 2^-126 flush to
-// zero, which no sum holding its max term can notice).
+// Softmax terms use the hardware v_exp_f32; results below 2^-126 flush to zero, which no
+// sum holding its max term can notice.  The running reference max of each query is moved
+// (and O and the sum rescaled) only when a tile's max exceeds it by more than 2^8, so exp
+// arguments are <= 8 and most tiles skip the rescale; the common factor cancels in the final
+// O / l.  The 1/sqrt(hd) scale (times log2 e) is folded into one FMA per score, and the
+// tile's key mask is applied only on a partial last tile (a scalar branch).
 // Everything is computed transposed with v_mfma_f32_16x16x32_bf16 so that a query's
 // softmax statistics never leave its lanes:
 //   S^T = K Q^T   (A = K tile from LDS, B = Q^T held in registers)
@@ -48,8 +52,9 @@ __global__ __launch_bounds__(256 * SPLIT, SB && SPLIT == 1 ? 3 : 1) void k_atten
   auto Vt = [&](int buf, int p) { return lds + NB * SPLIT * KSZ + (buf * SPLIT + p) * VSZ; };
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int part = wave >> 2;                // which part of the key range
-  const int tl = tid & 255, tpart = tid >> 8;  // loader thread: its index and part
+  // which part of the key range (wave-uniform, so tile indices and branches stay scalar)
+  const int part = __builtin_amdgcn_readfirstlane(wave >> 2);
+  const int tl = tid & 255, tpart = part;    // loader thread: its index and part
   const int bh = blockIdx.y, b = bh / H, h = bh % H, kvh = h / (H / Hkv);
   const int q0 = blockIdx.x * 64 + (wave & 3) * 16;
   const int g = lane >> 4, r16 = lane & 15;
@@ -66,22 +71,30 @@ __global__ __launch_bounds__(256 * SPLIT, SB && SPLIT == 1 ? 3 : 1) void k_atten
   f32x4_t o[HD / 16];
 #pragma unroll
   for (int d = 0; d < HD / 16; ++d) o[d] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  float m_run = -INFINITY, l_part = 0.f;
+  float m_ref = -INFINITY, l_part = 0.f;  // reference max (log2 units) and sum of this lane
+  constexpr float SLACK = 8.f;            // exp arguments stay <= SLACK
 
-  // K tile [64 keys][HD] and V^T tile [HD][64 keys] of part tpart: chunk c of this thread
-  // (pointers of key 0; a tile adds the uniform key0 * HD / key0)
+  // K tile [64 keys][HD] and V^T tile [HD][64 keys] of part tpart, read through buffer
+  // resources over this head's K and V^T: each chunk has a fixed per-lane byte offset and a
+  // tile adds the uniform key0 * HD * 2 (K) or key0 * 2 (V^T) as the scalar offset
   u32x4_t rk[CK], rv[CK];
+  const __amdgpu_buffer_rsrc_t k_rs =
+      __builtin_amdgcn_make_buffer_rsrc((void*)kh, (short)0, Ls * HD * 2, 0x00020000);
+  const __amdgpu_buffer_rsrc_t v_rs =
+      __builtin_amdgcn_make_buffer_rsrc((void*)vh, (short)0, HD * Ls * 2, 0x00020000);
   // chunk i of this thread: K row tl / (HD/8) + i * (256 / (HD/8)), V^T row tl / (KT/8) +
-  // i * (256 / (KT/8)); one lane offset per tensor, the rest uniform strides
-  const int koff = (tl / (HD / 8)) * HD + (tl % (HD / 8)) * 8;
-  const int voff = (tl / (KT / 8)) * Ls + (tl % (KT / 8)) * 8;
+  // i * (256 / (KT/8))
+  int kvo[CK], vvo[CK];
+#pragma unroll
+  for (int i = 0; i < CK; ++i) {
+    kvo[i] = ((tl / (HD / 8) + i * (256 / (HD / 8))) * HD + (tl % (HD / 8)) * 8) * 2;
+    vvo[i] = ((tl / (KT / 8) + i * (256 / (KT / 8))) * Ls + (tl % (KT / 8)) * 8) * 2;
+  }
   auto fetch = [&](int key0) {
-    const uint16_t* kb0 = kh + (int64_t)key0 * HD + koff;
-    const uint16_t* vb0 = vh + key0 + voff;
 #pragma unroll
     for (int i = 0; i < CK; ++i) {
-      rk[i] = *reinterpret_cast<const u32x4_t*>(kb0 + i * (256 / (HD / 8)) * HD);
-      rv[i] = *reinterpret_cast<const u32x4_t*>(vb0 + (int64_t)i * (256 / (KT / 8)) * Ls);
+      rk[i] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(k_rs, kvo[i], key0 * HD * 2, 0));
+      rv[i] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(v_rs, vvo[i], key0 * 2, 0));
     }
   };
   // K rows are stored in a permuted key order: tile key k = 32 a + 8 g + 4 b + i (a, b in
@@ -125,39 +138,37 @@ __global__ __launch_bounds__(256 * SPLIT, SB && SPLIT == 1 ? 3 : 1) void k_atten
           st[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[kk], st[kb], 0, 0, 0);
         }
       }
-      float tmax = -INFINITY;
-      if (key0 + KT <= L) {  // whole tile inside the sequence (uniform)
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            st[kb][i] *= scale_log2;
-            tmax = fmaxf(tmax, st[kb][i]);
-          }
-      } else {
+      if (key0 + KT > L) {  // partial last tile (scalar branch): keys past L drop out
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const int key = key0 + 32 * (kb >> 1) + 8 * g + 4 * (kb & 1) + i;
-            const float v = key < L ? st[kb][i] * scale_log2 : -INFINITY;
-            st[kb][i] = v;
-            tmax = fmaxf(tmax, v);
+            if (key >= L) st[kb][i] = -INFINITY;
           }
       }
+      float tmax = -INFINITY;  // raw scores: the scale is positive
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) tmax = fmaxf(tmax, st[kb][i]);
       tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
       tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-      const float m_new = fmaxf(m_run, tmax);
-      const float alpha = fast_exp2(m_run - m_new);  // 0 while m_run is -inf
-      m_run = m_new;
-      l_part *= alpha;
+      const float tm = tmax * scale_log2;
+      const bool grow = tm > m_ref + SLACK;  // true on a lane's first tile (m_ref = -inf)
+      if (__any(grow)) {
+        const float m_new = grow ? tm : m_ref;
+        const float alpha = fast_exp2(m_ref - m_new);  // 1 where kept, 0 while m_ref is -inf
+        m_ref = m_new;
+        l_part *= alpha;
 #pragma unroll
-      for (int d = 0; d < HD / 16; ++d) o[d] *= alpha;
+        for (int d = 0; d < HD / 16; ++d) o[d] *= alpha;
+      }
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const float p = fast_exp2(st[kb][i] - m_new);
+          const float p = fast_exp2(fmaf(st[kb][i], scale_log2, -m_ref));
           st[kb][i] = p;
           l_part += p;
         }
@@ -192,7 +203,7 @@ __global__ __launch_bounds__(256 * SPLIT, SB && SPLIT == 1 ? 3 : 1) void k_atten
     static_assert(sizeof(lds) >= (size_t)(SPLIT - 1) * 4 * NF * 64 * sizeof(float), "merge buffer");
     if (part > 0) {
       const int slot = ((part - 1) * 4 + (wave & 3)) * NF * 64 + lane;
-      comb[slot] = m_run;
+      comb[slot] = m_ref;
       comb[slot + 64] = l_part;
 #pragma unroll
       for (int d = 0; d < HD / 16; ++d)
@@ -205,9 +216,9 @@ __global__ __launch_bounds__(256 * SPLIT, SB && SPLIT == 1 ? 3 : 1) void k_atten
     for (int p = 1; p < SPLIT; ++p) {
       const int slot = ((p - 1) * 4 + (wave & 3)) * NF * 64 + lane;
       const float m1 = comb[slot], l1 = comb[slot + 64];
-      const float m = fmaxf(m_run, m1);
-      const float a0 = fast_exp2(m_run - m), a1 = fast_exp2(m1 - m);
-      m_run = m;
+      const float m = fmaxf(m_ref, m1);
+      const float a0 = fast_exp2(m_ref - m), a1 = fast_exp2(m1 - m);
+      m_ref = m;
       l_part = l_part * a0 + l1 * a1;
 #pragma unroll
       for (int d = 0; d < HD / 16; ++d)

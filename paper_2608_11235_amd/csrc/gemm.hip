@@ -102,8 +102,11 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void k_gemm(GemmArgs g) {
   // PIPE 2 stores every thread's chunks unconditionally: rows past the tile land in spare
   // LDS rows (CA * NT / 8 >= BM)
   constexpr int A_ROWS = PIPE == 2 ? CA * NT / 8 : BM, B_ROWS = PIPE == 2 ? CB * NT / 8 : BN;
-  __shared__ __attribute__((aligned(16))) uint16_t As[2][A_ROWS * LDK];
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][B_ROWS * LDK];
+  // one LDS array: the operand buffers As [2][A_ROWS * LDK] then Bs [2][B_ROWS * LDK]; the
+  // epilogues reuse it whole
+  __shared__ __attribute__((aligned(16))) uint16_t lds[2 * (A_ROWS + B_ROWS) * LDK];
+  auto As = reinterpret_cast<uint16_t(*)[A_ROWS * LDK]>(lds);
+  auto Bs = reinterpret_cast<uint16_t(*)[B_ROWS * LDK]>(lds + 2 * A_ROWS * LDK);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WAVES_N, wn = wave % WAVES_N;
@@ -319,42 +322,68 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void k_gemm(GemmArgs g) {
   // epilogue: acc[i][j][e] is C[row, col] with
   //   row = m0 + wm*TM*32 + i*32 + 8*(e/4) + 4*(lane/32) + e%4,  col = n0 + wn*TN*32 + j*32 + lane%32
   const int col_l = lane & 31, row_q = (lane >> 5) * 4;
+  // The bf16 epilogues (SwiGLU, QKV) stage each wavefront's finished tile in LDS (the
+  // operand buffers are free once every wavefront is past its last slice) and write it back
+  // as 16-byte stores: 128 contiguous bytes per row of q, k and the SwiGLU output, and per
+  // head dimension of the transposed v, instead of 2-byte stores spread over 32 rows.
+  constexpr int WR = TM * 32, WC = TN * 32;  // wavefront tile
   if constexpr (EPI == EPI_SWIGLU) {
-    uint16_t* C = reinterpret_cast<uint16_t*>(g.C);
+    constexpr int OC = WC / 2;                // output columns of the tile (gate/up pairs)
+    constexpr int SPS = OC + 8;               // staged row pitch, bf16
+    static_assert(sizeof(lds) >= (size_t)WAVES_M * WAVES_N * WR * SPS * 2, "stage");
+    __syncthreads();                          // every wavefront is done with As / Bs
+    uint16_t* scr = lds + wave * WR * SPS;
 #pragma unroll
-    for (int t = 0; t < TN / 2; ++t) {
-      const int pcol = n0 + wn * TN * 32 + t * 64;  // 64 physical columns: 32 gate, 32 up
-      if (pcol >= g.N) continue;
-      const int jcol = pcol / 2 + col_l;            // output (ffn) column
+    for (int t = 0; t < TN / 2; ++t)
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-          const int row = m0 + wm * TM * 32 + i * 32 + 8 * (e >> 2) + row_q + (e & 3);
-          if (row < g.M) {
-            const float gt = acc[i][2 * t][e], up = acc[i][2 * t + 1][e];
-            const float sg = gt / (1.0f + __expf(-gt));
-            C[(int64_t)row * g.ldc + jcol] = (uint16_t)f32_to_bf16_bits(sg * up);
-          }
+          const float gt = acc[i][2 * t][e], up = acc[i][2 * t + 1][e];
+          const float sg = gt / (1.0f + __expf(-gt));
+          scr[(i * 32 + 8 * (e >> 2) + row_q + (e & 3)) * SPS + t * 32 + col_l] =
+              (uint16_t)f32_to_bf16_bits(sg * up);
         }
+    __syncthreads();
+    uint16_t* C = reinterpret_cast<uint16_t*>(g.C);
+    const int pcol0 = n0 + wn * WC;           // first physical column of the wavefront
+    const int jcol0 = pcol0 / 2;              // its first output (ffn) column
+    const int ncol = min(OC, (g.N - pcol0) / 2);
+    constexpr int CPR = OC / 8;               // 16-byte chunks per staged row
+    const int64_t row0 = m0 + wm * WR;
+    if (ncol > 0) {
+#pragma unroll
+      for (int k = 0; k < WR * CPR / 64; ++k) {
+        const int id = lane + 64 * k, r = id / CPR, cc = (id % CPR) * 8;
+        if (row0 + r < g.M && cc < ncol)
+          *reinterpret_cast<u32x4_t*>(C + (row0 + r) * g.ldc + jcol0 + cc) =
+              *reinterpret_cast<const u32x4_t*>(scr + r * SPS + cc);
+      }
     }
   } else if constexpr (EPI == EPI_QKV_ROPE) {
     // q/k columns are pair-interleaved within a head, so the rotate-half partner of
-    // column c is column c ^ 1, held by lane ^ 1 for the same rows.  A lane's rows come in
-    // groups of 4 consecutive rows: one division per group, and v (stored transposed) is
-    // written as 4 consecutive positions at once when the group stays in one sequence.
+    // column c is column c ^ 1, held by lane ^ 1 for the same rows.  A wavefront's WC
+    // columns lie in one head of one section (q, k or v): section widths are multiples of
+    // 64.  q and k are staged row-major and leave as rows of the head layout; v is staged
+    // transposed and leaves as runs of 8 positions of the transposed layout.
     const QkvOut& o = g.qkv;
     const int hd = o.head_dim, half = hd / 2;
     const int hq = o.n_heads * hd, hkv = o.n_kv_heads * hd;
+    const int c0 = n0 + wn * WC;
+    const int sec = c0 < hq ? 0 : (c0 < hq + hkv ? 1 : 2);
+    const int cc0 = c0 - (sec == 0 ? 0 : (sec == 1 ? hq : hq + hkv));
+    const int head = cc0 / hd, pd0 = cc0 % hd;
+    constexpr int SPS = WC + 8, SPV = WR + 8;  // staged pitches, bf16
+    static_assert(sizeof(lds) >= (size_t)WAVES_M * WAVES_N * WR * SPS * 2 &&
+                  sizeof(lds) >= (size_t)WAVES_M * WAVES_N * WC * SPV * 2, "stage");
+    __syncthreads();                           // every wavefront is done with As / Bs
+    uint16_t* scr = lds + wave * (WR * SPS > WC * SPV ? WR * SPS : WC * SPV);
+    const int64_t row0 = m0 + wm * WR;
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
-      const int col = n0 + wn * TN * 32 + j * 32 + col_l;
-      const bool in = col < g.N;
-      const float bias = (in && g.bias) ? g.bias[col] : 0.f;
-      const int sec = col < hq ? 0 : (col < hq + hkv ? 1 : 2);
-      const int cc = col - (sec == 0 ? 0 : (sec == 1 ? hq : hq + hkv));
-      const int head = cc / hd, pd = cc % hd;
-      const int ii = pd >> 1;
+      const int col = c0 + j * 32 + col_l;
+      const float bias = (col < g.N && g.bias) ? g.bias[col] : 0.f;
+      const int ii = (pd0 + j * 32 + col_l) >> 1;
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -367,66 +396,72 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void k_gemm(GemmArgs g) {
               x[u][t] = acc[i][j][(2 * hf + u) * 4 + t] + bias;
               partner[u][t] = __shfl_xor(x[u][t], 1, 64);
             }
-          if (!in) continue;
-          const int rbase = m0 + wm * TM * 32 + i * 32 + row_q + 16 * hf;
-          if (sec < 2) {
-            // the cos/sin loads of these 8 elements are issued before their first store: a
-            // load behind a store would also wait for that store
-            float cs[2][4], sn[2][4];
-#pragma unroll
-            for (int u = 0; u < 2; ++u) {
-              const int row0 = rbase + 8 * u;
-              int pos = row0 - row0 / o.L * o.L;
-#pragma unroll
-              for (int t = 0; t < 4; ++t) {
-                if (row0 + t < g.M) {
-                  cs[u][t] = o.cos_t[pos * half + ii];
-                  sn[u][t] = o.sin_t[pos * half + ii];
-                }
-                if (++pos == o.L) pos = 0;
-              }
-            }
-#pragma unroll
-            for (int u = 0; u < 2; ++u) {
-              const int row0 = rbase + 8 * u;
-              if (row0 >= g.M) continue;
-              int b = row0 / o.L, pos = row0 - b * o.L;
-#pragma unroll
-              for (int t = 0; t < 4; ++t) {
-                if (row0 + t >= g.M) break;
-                const float r = (pd & 1) ? x[u][t] * cs[u][t] + partner[u][t] * sn[u][t]
-                                         : x[u][t] * cs[u][t] - partner[u][t] * sn[u][t];
-                uint16_t* dst = sec == 0
-                                    ? o.q + ((int64_t)(b * o.n_heads + head) * o.Ls + pos) * hd
-                                    : o.k + ((int64_t)(b * o.n_kv_heads + head) * o.Ls + pos) * hd;
-                dst[pd] = (uint16_t)f32_to_bf16_bits(r);
-                if (++pos == o.L) { pos = 0; ++b; }
-              }
-            }
-            continue;
-          }
 #pragma unroll
           for (int u = 0; u < 2; ++u) {
-            const int row0 = rbase + 8 * u;
-            if (row0 >= g.M) continue;
-            int b = row0 / o.L, pos = row0 - b * o.L;
-            if (pos + 3 < o.L && row0 + 3 < g.M && (o.L & 3) == 0) {
+            const int rl = i * 32 + row_q + 16 * hf + 8 * u;  // staged row of element t = 0
+            if (sec < 2) {
+              // the cos/sin loads of these 4 elements are issued before the LDS writes
+              float cs[4], sn[4];
+              int pos = (int)((row0 + rl) % o.L);
+#pragma unroll
+              for (int t = 0; t < 4; ++t) {
+                cs[t] = o.cos_t[pos * half + ii];
+                sn[t] = o.sin_t[pos * half + ii];
+                if (++pos == o.L) pos = 0;
+              }
+#pragma unroll
+              for (int t = 0; t < 4; ++t) {
+                const float r = (col_l & 1) ? x[u][t] * cs[t] + partner[u][t] * sn[t]
+                                            : x[u][t] * cs[t] - partner[u][t] * sn[t];
+                scr[(rl + t) * SPS + j * 32 + col_l] = (uint16_t)f32_to_bf16_bits(r);
+              }
+            } else {
               u32x2_t v2;
               v2.x = pack_bf16x2(x[u][0], x[u][1]);
               v2.y = pack_bf16x2(x[u][2], x[u][3]);
-              *reinterpret_cast<u32x2_t*>(
-                  &o.vt[((int64_t)(b * o.n_kv_heads + head) * hd + pd) * o.Ls + pos]) = v2;
-              continue;
-            }
-#pragma unroll
-            for (int t = 0; t < 4; ++t) {
-              if (row0 + t >= g.M) break;
-              o.vt[((int64_t)(b * o.n_kv_heads + head) * hd + pd) * o.Ls + pos] =
-                  (uint16_t)f32_to_bf16_bits(x[u][t]);
-              if (++pos == o.L) { pos = 0; ++b; }
+              *reinterpret_cast<u32x2_t*>(scr + (j * 32 + col_l) * SPV + rl) = v2;
             }
           }
         }
+    }
+    __syncthreads();
+    if (c0 < g.N) {
+      if (sec < 2) {
+        constexpr int CPR = WC / 8;            // 16-byte chunks per staged row
+        uint16_t* base = sec == 0 ? o.q : o.k;
+        const int nh = sec == 0 ? o.n_heads : o.n_kv_heads;
+#pragma unroll
+        for (int k = 0; k < WR * CPR / 64; ++k) {
+          const int id = lane + 64 * k, r = id / CPR, cc = (id % CPR) * 8;
+          const int64_t m = row0 + r;
+          if (m < g.M) {
+            const int b = (int)(m / o.L), pos = (int)(m - (int64_t)b * o.L);
+            *reinterpret_cast<u32x4_t*>(base + ((int64_t)(b * nh + head) * o.Ls + pos) * hd +
+                                        pd0 + cc) =
+                *reinterpret_cast<const u32x4_t*>(scr + r * SPS + cc);
+          }
+        }
+      } else {
+        constexpr int CPC = WR / 8;            // runs of 8 positions per head dimension
+#pragma unroll
+        for (int k = 0; k < WC * CPC / 64; ++k) {
+          const int id = lane + 64 * k, dcol = id / CPC, rr = (id % CPC) * 8;
+          const int64_t m = row0 + rr;
+          const int b = (int)(m / o.L), pos = (int)(m - (int64_t)b * o.L);
+          uint16_t* dst = o.vt + ((int64_t)(b * o.n_kv_heads + head) * hd + pd0 + dcol) * o.Ls;
+          if (m + 7 < g.M && pos + 7 < o.L && (pos & 7) == 0) {
+            *reinterpret_cast<u32x4_t*>(dst + pos) =
+                *reinterpret_cast<const u32x4_t*>(scr + dcol * SPV + rr);
+          } else {
+            int bb = b, pp = pos;
+            for (int t = 0; t < 8 && m + t < g.M; ++t) {
+              o.vt[((int64_t)(bb * o.n_kv_heads + head) * hd + pd0 + dcol) * o.Ls + pp] =
+                  scr[dcol * SPV + rr + t];
+              if (++pp == o.L) { pp = 0; ++bb; }
+            }
+          }
+        }
+      }
     }
   } else if constexpr (EPI == EPI_TOP1) {
     // Row statistics of Eq. (1) over this wavefront's TN x 32 columns.  Each 32 x 32 block
@@ -435,9 +470,9 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void k_gemm(GemmArgs g) {
     // of a row are merged (lower columns first), and the blocks of a block row are folded in
     // column order.
     constexpr int SP = 34;  // scratch row pitch, bf16
-    static_assert(sizeof(As) >= (size_t)WAVES_M * WAVES_N * 32 * SP * 2, "TOP1 scratch");
+    static_assert(sizeof(lds) >= (size_t)WAVES_M * WAVES_N * 32 * SP * 2, "TOP1 scratch");
     __syncthreads();  // every wavefront is done reading the operand tiles
-    uint16_t* scr = &As[0][0] + wave * 32 * SP;
+    uint16_t* scr = lds + wave * 32 * SP;
     const int rr = lane & 31, half = lane >> 5;
     TopState rs[TM];
 #pragma unroll
@@ -517,28 +552,34 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void k_gemm(GemmArgs g) {
 // cfg 1:  32 x 128 tile, 4 waves (1 x 4) (2 waves for SwiGLU), for M <= 64 (LM head rows)
 // cfg 2: 256 x 128 tile,  8 waves (4 x 2), wave tile 64 x 64, PIPE 2
 // cfg 3: 256 x 192 tile, 12 waves (4 x 3), wave tile 64 x 64, PIPE 2
+// cfg 4: 128 x 192 tile,  6 waves (2 x 3), wave tile 64 x 64, PIPE 2: twice the tiles of
+//        cfg 3, so an output of 512 rows x 12288 columns fills 256 CUs without splitting K
 struct CfgShape { int bm, bn; };
 static CfgShape cfg_shape(int cfg) {
   switch (cfg) {
     case 0: return {256, 256};
     case 1: return {32, 128};
     case 3: return {256, 192};
+    case 4: return {128, 192};
     default: return {256, 128};
   }
 }
 
-int gemm_num_cfgs() { return 4; }
+int gemm_num_cfgs() { return 5; }
 
 // wavefront columns per tile and their width (TN x 32) of each config
 int gemm_top1_parts(const GemmPlan& p, int N) {
   const CfgShape sh = cfg_shape(p.cfg);
-  const int waves_n = p.cfg == 0 ? 4 : (p.cfg == 1 ? 4 : (p.cfg == 3 ? 3 : 2));
+  const int waves_n = p.cfg == 0 ? 4 : (p.cfg == 1 ? 4 : (p.cfg == 3 || p.cfg == 4 ? 3 : 2));
   return (N + sh.bn - 1) / sh.bn * waves_n;
 }
 
-// Relative main-loop efficiency of the large-tile configs (16, 12 and 8 waves per workgroup),
-// measured on the pass's shapes.
-static double cfg_eff(int cfg) { return cfg == 0 ? 1.0 : (cfg == 3 ? 1.03 : 0.88); }
+// Relative main-loop efficiency of the large-tile configs (16, 12, 8 and 6 waves per
+// workgroup), measured on the pass's shapes (cfg 4: 64.4 us for the whole-K QKV projection
+// with its bias + RoPE epilogue at 512 x 12288 x 4096).
+static double cfg_eff(int cfg) {
+  return cfg == 0 ? 1.0 : (cfg == 3 ? 1.03 : (cfg == 4 ? 0.72 : 0.88));
+}
 
 GemmPlan gemm_plan_cfg(int M, int N, int K, int cfg, int splits) {
   GemmPlan p{};
@@ -555,10 +596,10 @@ GemmPlan gemm_plan_cfg(int M, int N, int K, int cfg, int splits) {
 // 256 x 128 for 512 x 12288).
 GemmPlan gemm_plan(int M, int N, int K, int num_cus) {
   if (M <= 64) return gemm_plan_cfg(M, N, K, 1, 1);
-  const int cfgs[3] = {0, 3, 2};
+  const int cfgs[4] = {0, 3, 2, 4};
   int best = 0;
   double best_cost = 0;
-  for (int c = 0; c < 3; ++c) {
+  for (int c = 0; c < 4; ++c) {
     const CfgShape sh = cfg_shape(cfgs[c]);
     const int tiles = ((M + sh.bm - 1) / sh.bm) * ((N + sh.bn - 1) / sh.bn);
     const int rounds = (tiles + num_cus - 1) / num_cus;
@@ -570,17 +611,18 @@ GemmPlan gemm_plan(int M, int N, int K, int num_cus) {
 
 // Tiles that may split K (outputs whose consumer folds partials in): estimated time =
 // rounds x per-tile main loop (2.18 MMAC per microsecond per CU at efficiency 1) + partial
-// traffic (written here, read back downstream: ~0.4 us per MiB), over configs {0, 2, 3} and
+// traffic (written here, read back downstream: ~0.46 us per MiB, the measured cost of the
+// QKV split-K 2 partials and their finish kernel), over configs {0, 2, 3, 4} and
 // 1, 2, 4 or 8 splits with >= 8 K-slices each (only `splits` when it is > 0).  Splits never
 // exceed the workspace bound.
 GemmPlan gemm_plan_split(int M, int N, int K, int num_cus, int splits) {
   if (M <= 64 && splits <= 1) return gemm_plan_cfg(M, N, K, 1, 1);
   const int nk = K / BK;
-  const int cfgs[3] = {0, 3, 2};
+  const int cfgs[4] = {0, 3, 2, 4};
   GemmPlan best{};
   double best_us = 0;
   bool have = false;
-  for (int c = 0; c < 3; ++c) {
+  for (int c = 0; c < 4; ++c) {
     const CfgShape sh = cfg_shape(cfgs[c]);
     const int tiles = ((M + sh.bm - 1) / sh.bm) * ((N + sh.bn - 1) / sh.bn);
     for (int sp = 1; sp <= 8; sp *= 2) {
@@ -590,7 +632,7 @@ GemmPlan gemm_plan_split(int M, int N, int K, int num_cus, int splits) {
         continue;
       const int rounds = (tiles * sp + num_cus - 1) / num_cus;
       double us = (double)rounds * sh.bm * sh.bn * ((double)K / sp) / cfg_eff(cfgs[c]) / 2.18e6;
-      if (sp > 1) us += 0.4 * (double)sp * M * N * 4.0 / (1 << 20);
+      if (sp > 1) us += 0.46 * (double)sp * M * N * 4.0 / (1 << 20);
       if (!have || us < best_us) { best = gemm_plan_cfg(M, N, K, cfgs[c], sp); best_us = us; have = true; }
     }
   }
@@ -619,6 +661,7 @@ static hipError_t run_cfg(int cfg, const GemmArgs& a, int grid, hipStream_t s, h
       if constexpr (EPI == EPI_SWIGLU) return run<1, 2, 1, 2, EPI, 1>(a, grid, s, e0, e1);
       else return run<1, 4, 1, 1, EPI, 1>(a, grid, s, e0, e1);
     case 3: return run<4, 3, 2, 2, EPI, 2>(a, grid, s, e0, e1);
+    case 4: return run<2, 3, 2, 2, EPI, 2>(a, grid, s, e0, e1);
     default: return run<4, 2, 2, 2, EPI, 2>(a, grid, s, e0, e1);
   }
 }

@@ -8,22 +8,23 @@ namespace cora {
 
 // One workgroup per row: fold the split-K partials of a residual GEMM into h (in split
 // order, so the sum does not depend on scheduling), then normalise the updated row for the
-// next GEMM.  Row values stay in registers between the two phases.  SPLITS and the chunk
-// count C (float4 chunks per thread, C * 1024 >= d) are compile-time, so every partial and
-// residual load of a thread is issued before the first add.
-template <int SPLITS, int C>
-__global__ __launch_bounds__(256) void k_residual_norm(float* __restrict__ h,
-                                                       const float* __restrict__ part,
-                                                       int64_t slab, int d,
-                                                       const float* __restrict__ w,
-                                                       uint16_t* __restrict__ out, float eps) {
+// next GEMM.  Row values stay in registers between the two phases.  SPLITS, the threads NT
+// and the chunk count C (float4 chunks per thread, C * NT * 4 >= d) are compile-time, so
+// every partial and residual load of a thread is issued before the first add; rows of
+// 4096 take 1024 threads with one chunk each, which keeps the most loads in flight.
+template <int SPLITS, int C, int NT>
+__global__ __launch_bounds__(NT) void k_residual_norm(float* __restrict__ h,
+                                                      const float* __restrict__ part,
+                                                      int64_t slab, int d,
+                                                      const float* __restrict__ w,
+                                                      uint16_t* __restrict__ out, float eps) {
   const int64_t r = blockIdx.x;
   float* x = h + r * d;
   const float* p = part + r * d;
   float4 pv[C][SPLITS], v[C];
 #pragma unroll
   for (int i = 0; i < C; ++i) {
-    const int c = (threadIdx.x + i * 256) * 4;
+    const int c = (threadIdx.x + i * NT) * 4;
     if (c < d) {
 #pragma unroll
       for (int sp = 0; sp < SPLITS; ++sp) pv[i][sp] = *reinterpret_cast<const float4*>(p + sp * slab + c);
@@ -33,7 +34,7 @@ __global__ __launch_bounds__(256) void k_residual_norm(float* __restrict__ h,
   float ss = 0.f;
 #pragma unroll
   for (int i = 0; i < C; ++i) {
-    const int c = (threadIdx.x + i * 256) * 4;
+    const int c = (threadIdx.x + i * NT) * 4;
     if (c < d) {
       float4 acc = pv[i][0];
 #pragma unroll
@@ -53,15 +54,17 @@ __global__ __launch_bounds__(256) void k_residual_norm(float* __restrict__ h,
   }
   if (!out) return;
   ss = warp_sum(ss);
-  __shared__ float red[4];
+  __shared__ float red[NT / 64];
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
   __syncthreads();
-  const float tot = red[0] + red[1] + red[2] + red[3];
+  float tot = 0.f;
+#pragma unroll
+  for (int i = 0; i < NT / 64; ++i) tot += red[i];
   const float inv = 1.0f / sqrtf(tot / (float)d + eps);
   uint16_t* o = out + r * d;
 #pragma unroll
   for (int i = 0; i < C; ++i) {
-    const int c = (threadIdx.x + i * 256) * 4;
+    const int c = (threadIdx.x + i * NT) * 4;
     if (c < d) {
       const float4 g = *reinterpret_cast<const float4*>(w + c);
       u32x2_t q;
@@ -73,13 +76,13 @@ __global__ __launch_bounds__(256) void k_residual_norm(float* __restrict__ h,
 }
 
 template <int SPLITS>
-static void residual_norm_c(int C, dim3 grid, hipStream_t s, float* h, const float* part,
+static void residual_norm_c(int d4, dim3 grid, hipStream_t s, float* h, const float* part,
                             int64_t slab, int d, const float* w, uint16_t* out, float eps) {
-#define RN(C_) hipLaunchKernelGGL((k_residual_norm<SPLITS, C_>), grid, dim3(256), 0, s, h, part, slab, d, w, out, eps)
-  if (C <= 1) RN(1);
-  else if (C <= 2) RN(2);
-  else if (C <= 4) RN(4);
-  else RN(8);
+#define RN(C_, NT_) hipLaunchKernelGGL((k_residual_norm<SPLITS, C_, NT_>), grid, dim3(NT_), 0, s, h, part, slab, d, w, out, eps)
+  if (d4 <= 256) RN(1, 256);
+  else if (d4 <= 512) RN(1, 512);
+  else if (d4 <= 1024) RN(1, 1024);
+  else RN(2, 1024);
 #undef RN
 }
 
@@ -87,15 +90,15 @@ hipError_t launch_residual_norm(float* h, const float* part, int splits, int row
                                 const float* w, uint16_t* out, float eps, hipStream_t s) {
   if (rows == 0) return hipSuccess;
   if (d % 4 != 0 || d > RESIDUAL_NORM_MAX_D) return hipErrorInvalidValue;
-  static_assert(RESIDUAL_NORM_MAX_D <= 8 * 1024, "at most 8 float4 chunks per thread");
-  const int C = (d + 1023) / 1024;
+  static_assert(RESIDUAL_NORM_MAX_D <= 2 * 1024 * 4, "at most 2 float4 chunks per thread");
+  const int d4 = d / 4;
   const int64_t slab = (int64_t)rows * d;
   const dim3 grid(rows);
   switch (splits) {
-    case 1: residual_norm_c<1>(C, grid, s, h, part, slab, d, w, out, eps); break;
-    case 2: residual_norm_c<2>(C, grid, s, h, part, slab, d, w, out, eps); break;
-    case 4: residual_norm_c<4>(C, grid, s, h, part, slab, d, w, out, eps); break;
-    case 8: residual_norm_c<8>(C, grid, s, h, part, slab, d, w, out, eps); break;
+    case 1: residual_norm_c<1>(d4, grid, s, h, part, slab, d, w, out, eps); break;
+    case 2: residual_norm_c<2>(d4, grid, s, h, part, slab, d, w, out, eps); break;
+    case 4: residual_norm_c<4>(d4, grid, s, h, part, slab, d, w, out, eps); break;
+    case 8: residual_norm_c<8>(d4, grid, s, h, part, slab, d, w, out, eps); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
