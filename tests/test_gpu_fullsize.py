@@ -113,6 +113,10 @@ def _teacher_forced_spot_steps(n_layers, range_case):
     spec = si.LLADA_8B.with_layers(n_layers)
     P, G, BLK, S = 256, 256, 32, 32
     w = si.HostWeights(spec, 0)
+    for i in range(n_layers):                       # seeded host weights, with progress
+        w.layer(i)
+        if i % 8 == 7:
+            print(f"    host weights: layer {i + 1} of {n_layers}", flush=True)
     gate = Gate(0.65, 1, True)
     tot = {"top1": 0, "dec": 0, "rows": 0, "U": 0, "own": 0, "own_U": 0}
     with Model(spec, seed=0, max_batch=1, max_seq=P + G) as m:
