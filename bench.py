@@ -36,8 +36,8 @@ TIME_EVERY = 4              # gate/up event timing on every 4th timed pass
 # file and the shared device headers.
 SHARED_SOURCES = ("paper_2608_11235_amd/csrc/common.hpp", "paper_2608_11235_amd/csrc/internal.hpp")
 COUNTER_TRAFFIC = {
-    "gate_up": ("paper_2608_11235_amd/csrc/gemm.hip", "f98a384cb63fd75d", 247624449),
-    "vocab_gate": ("paper_2608_11235_amd/csrc/vocab_gate.hip", "b83e656124978083", 1036531324),
+    "gate_up": ("paper_2608_11235_amd/csrc/gemm.hip", "21ee07e23f752184", 247629209),
+    "vocab_gate": ("paper_2608_11235_amd/csrc/vocab_gate.hip", "8158577e35d7c498", 1036529255),
 }
 
 
@@ -372,6 +372,39 @@ def table3_sweep_leg(logit_scale=8.0):
     return out
 
 
+def shape_passes_leg(passes=6, warmup=2):
+    """Per-pass wall-clock timing of whole denoising steps at the Dream-7B B = 8 and LLaDA-8B
+    L = 1280 shapes (a short run for kernel traces of those shapes; the decode legs time the
+    full decodes)."""
+    import torch
+
+    import seeded_inputs as si
+    from paper_2608_11235_amd import DecodeState, Gate, Model, Sched
+
+    out = {}
+    for name, spec, b, p, g in (("dream7b_b8_gen256", si.DREAM_7B, 8, 256, 256),
+                                ("llada8b_gen1024", si.LLADA_8B, 1, 256, 1024)):
+        prompt = si.prompt_tokens(1, b, p, spec.vocab, spec.mask_id)
+        sched, gate = Sched(BLK, S), Gate(DELTA_P, M_REQ, True)
+        with Model(spec, seed=0, max_batch=b, max_seq=p + g) as m:
+            st = DecodeState.from_host(si.initial_decode_state(prompt, g, spec.mask_id), p, g,
+                                       BLK, BLK, device="cuda")
+            for _ in range(warmup):
+                m.denoise_step(st, sched, gate)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for _ in range(passes):
+                m.denoise_step(st, sched, gate)
+            torch.cuda.synchronize()
+            dt = (time.perf_counter() - t0) / passes
+        fl = pass_flops(spec, b * (p + g), b * BLK, batch=b)
+        out[name] = {"passes_timed": passes, "ms_per_pass": round(dt * 1e3, 3),
+                     "pass_mfma_frac": round(fl / dt / 1e12 / PEAK_BF16_TFLOPS, 4)}
+        torch.cuda.empty_cache()
+        note(f"shape passes {name} done")
+    return out
+
+
 def copy_calibration(nbytes=1 << 30, iters=5):
     """A plain device-to-device copy of known size: reference for HBM byte counters."""
     import torch
@@ -409,7 +442,7 @@ def main():
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the labelled logits-x8 gate-variant sweep")
     ap.add_argument("--only", choices=["all", "pass", "vocab", "copy", "gated", "compaction",
-                                       "shapes", "sweep", "cpu"],
+                                       "shapes", "shape-passes", "sweep", "cpu"],
                     default="all",
                     help="run one leg only (profiling runs): the timed passes, the vocab/gate "
                          "kernel, or a plain 1 GiB device copy that calibrates byte counters")
@@ -428,6 +461,9 @@ def main():
         return
     if args.only == "shapes":
         print(json.dumps(shape_legs()), flush=True)
+        return
+    if args.only == "shape-passes":
+        print(json.dumps({"shape_passes": shape_passes_leg()}), flush=True)
         return
     if args.only == "sweep":
         print(json.dumps({"table3_sweep_logits_x8": table3_sweep_leg()}), flush=True)
