@@ -114,5 +114,7 @@ def test_disagreement_losses_and_ratio():
     Y = np.array([5, 6, 7, 8])
     assert theory.accepted_disagreement([], [], Y) == 0.0
     assert theory.accepted_disagreement([0, 2], [5, 1], Y) == 0.5
+    # one of three accepted tokens differs: 1/3, which no count of agreements gives
+    assert theory.accepted_disagreement([0, 1, 2], [5, 6, 1], Y) == pytest.approx(1 / 3)
     assert theory.output_disagreement([5, 6, 0, 0], Y) == 0.5
     assert theory.step_ratio([3, 4], [32, 32]) == pytest.approx(7 / 64)
