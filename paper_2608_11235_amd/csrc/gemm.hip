@@ -322,10 +322,11 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void k_gemm(GemmArgs g) {
   // epilogue: acc[i][j][e] is C[row, col] with
   //   row = m0 + wm*TM*32 + i*32 + 8*(e/4) + 4*(lane/32) + e%4,  col = n0 + wn*TN*32 + j*32 + lane%32
   const int col_l = lane & 31, row_q = (lane >> 5) * 4;
-  // The bf16 epilogues (SwiGLU, QKV) stage each wavefront's finished tile in LDS (the
+  // The SwiGLU, QKV and fp32 epilogues stage each wavefront's finished tile in LDS (the
   // operand buffers are free once every wavefront is past its last slice) and write it back
-  // as 16-byte stores: 128 contiguous bytes per row of q, k and the SwiGLU output, and per
-  // head dimension of the transposed v, instead of 2-byte stores spread over 32 rows.
+  // as 16-byte stores: 128 contiguous bytes per row of q, k and the SwiGLU output, per head
+  // dimension of the transposed v and per 32 floats of an fp32 row, instead of 2- or 4-byte
+  // stores spread over 32 rows.
   constexpr int WR = TM * 32, WC = TN * 32;  // wavefront tile
   if constexpr (EPI == EPI_SWIGLU) {
     constexpr int OC = WC / 2;                // output columns of the tile (gate/up pairs)
@@ -516,29 +517,66 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void k_gemm(GemmArgs g) {
         g.part_arg[o] = rs[i].arg;
       }
     }
+  } else if constexpr (EPI == EPI_ADD_F32 || EPI == EPI_PART_F32) {
+    // fp32 outputs (residual update, split-K partials): each wavefront stages one 32-row
+    // block of its tile at a time in LDS (a whole fp32 tile per wavefront would not fit) and
+    // writes rows of WC floats as 16-byte stores, a read-modify-write for the residual update
+    constexpr int SPF = WC + 4;                // staged row pitch, fp32
+    constexpr int CPR = WC / 4;                // 16-byte chunks per staged row
+    static_assert(sizeof(lds) >= (size_t)WAVES_M * WAVES_N * 32 * SPF * 4, "stage");
+    float* scr = reinterpret_cast<float*>(lds) + wave * 32 * SPF;
+    float* C = reinterpret_cast<float*>(g.C) +
+               (EPI == EPI_PART_F32 ? (int64_t)split * g.M * g.ldc : (int64_t)0);
+    const int c0 = n0 + wn * WC;
+    const int ncol = min(WC, g.N - c0);
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      __syncthreads();  // the operand buffers (i = 0) or the previous block are done with
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int e = 0; e < 16; ++e)
+          scr[(8 * (e >> 2) + row_q + (e & 3)) * SPF + j * 32 + col_l] = acc[i][j][e];
+      __syncthreads();
+      const int64_t row0 = m0 + wm * WR + i * 32;
+      if (ncol > 0) {
+#pragma unroll
+        for (int k = 0; k < 32 * CPR / 64; ++k) {
+          const int id = lane + 64 * k, r = id / CPR, cc = (id % CPR) * 4;
+          if (row0 + r >= g.M || cc >= ncol) continue;
+          float* dst = C + (row0 + r) * g.ldc + c0 + cc;
+          const float* src = scr + r * SPF + cc;
+          if (cc + 4 <= ncol) {
+            float4 v = *reinterpret_cast<const float4*>(src);
+            if constexpr (EPI == EPI_ADD_F32) {
+              const float4 h = *reinterpret_cast<const float4*>(dst);
+              v.x = h.x + v.x;
+              v.y = h.y + v.y;
+              v.z = h.z + v.z;
+              v.w = h.w + v.w;
+            }
+            *reinterpret_cast<float4*>(dst) = v;
+          } else {
+            for (int t = 0; t < ncol - cc; ++t) dst[t] = EPI == EPI_ADD_F32 ? dst[t] + src[t] : src[t];
+          }
+        }
+      }
+    }
   } else {
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
       const int col = n0 + wn * TN * 32 + j * 32 + col_l;
       if (col >= g.N) continue;
-      const float bias = (EPI == EPI_BF16 && g.bias) ? g.bias[col] : 0.f;
+      const float bias = g.bias ? g.bias[col] : 0.f;
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int row = m0 + wm * TM * 32 + i * 32 + 8 * (e >> 2) + row_q + (e & 3);
           if (row >= g.M) continue;
-          if constexpr (EPI == EPI_ADD_F32) {
-            float* C = reinterpret_cast<float*>(g.C);
-            C[(int64_t)row * g.ldc + col] += acc[i][j][e];
-          } else if constexpr (EPI == EPI_PART_F32) {
-            float* C = reinterpret_cast<float*>(g.C) + (int64_t)split * g.M * g.ldc;
-            C[(int64_t)row * g.ldc + col] = acc[i][j][e];
-          } else {
-            uint16_t* C = reinterpret_cast<uint16_t*>(g.C);
-            C[(int64_t)row * g.ldc + col] =
-                (uint16_t)f32_to_bf16_bits((acc[i][j][e] + bias) * g.scale);
-          }
+          uint16_t* C = reinterpret_cast<uint16_t*>(g.C);
+          C[(int64_t)row * g.ldc + col] =
+              (uint16_t)f32_to_bf16_bits((acc[i][j][e] + bias) * g.scale);
         }
     }
   }
