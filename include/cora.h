@@ -160,10 +160,12 @@ cora_status cora_model_destroy(cora_model *model);
 
 /* Dense forward pass over tokens [B, L] (int32, device) and the LM head on
  * canvas rows [row_begin, row_begin + n_rows) of every batch row: writes
- * bf16 logits [B, n_rows, V] (device, caller-allocated).  Up to 64 rows
- * (B * n_rows) go through the few-row LM-head kernel, more through the tiled
+ * bf16 logits [B, n_rows, V] (device, caller-allocated).  When
+ * max_batch * n_rows <= 64 the few-row LM-head kernel runs, else the tiled
  * GEMM; both round (sum_k a_k w_k) * logit_scale to bf16 and differ only in
- * fp32 summation order.  Parity hook. */
+ * fp32 summation order.  Every kernel choice that sets a summation order is
+ * made for max_batch rows, so a row's logits do not depend on B.  Parity
+ * hook. */
 cora_status cora_forward_logits(cora_model *model, const int32_t *d_tokens, int32_t B, int32_t L,
                                 int32_t row_begin, int32_t n_rows, uint16_t *d_logits,
                                 void *hip_stream);
@@ -174,12 +176,13 @@ cora_status cora_forward_logits(cora_model *model, const int32_t *d_tokens, int3
  * see cora_vocab_gate).  top1/conf are [B, block_len] (the active block's
  * rows) under the BLOCK scope and [B, gen_len] (the generation region, LM head
  * and row reduction in chunks of up to 256 rows) under GLOBAL.  Eq. (1) is
- * computed inside the LM-head pass and no logits are written: a call (or
- * chunk) that scores at most 64 rows in all streams the packed weight copy
- * (per-128-entry partial max / first arg max / sum of exp), more rows reduce
- * each wavefront's logit columns in the tiled GEMM's epilogue; the partials
- * are merged in vocab order.  The top-1 is then the same as cora_vocab_gate's
- * on the logits cora_forward_logits writes for those rows (same row count).
+ * computed inside the LM-head pass and no logits are written: when max_batch
+ * times the rows scored per batch row (per chunk) is at most 64, the pass
+ * streams the packed weight copy (per-128-entry partial max / first arg max /
+ * sum of exp), else each wavefront's logit columns are reduced in the tiled
+ * GEMM's epilogue; the partials are merged in vocab order.  The top-1 is then
+ * the same as cora_vocab_gate's on the logits cora_forward_logits writes for
+ * those rows, at any B (the kernel choices are made for max_batch).
  * Only a vocabulary too small for the partials to fit the logits buffer takes
  * logits + row reduction.  Asynchronous. */
 cora_status cora_denoise_step(cora_model *model, cora_state *state, const cora_sched_cfg *sched,
