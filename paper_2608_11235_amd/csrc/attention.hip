@@ -14,7 +14,17 @@
 // barrier per tile).  Large grids (SB) keep one LDS tile buffer and at most 168 registers,
 // so three workgroups share a CU (three wavefronts per SIMD instead of two): each
 // wavefront's per-tile chain (MFMAs, max, lane exchange, exp, MFMAs) is latency-bound, and
-// the third wavefront hides more of it than the second barrier per tile costs.
+// the third wavefront hides more of it than the second barrier per tile costs.  Within a
+// tile, the K fragments are read in two batches of 8 (one LDS round trip per batch rather
+// than one per MFMA pair) and the first half of the V^T fragments is read before the
+// softmax, whose VALU work then covers that round trip.
+// LDS rows are padded to 288 bytes (K) and 160 bytes (V^T).  A 16-byte LDS read serves
+// the 32 lanes of each wavefront half from one 512-byte bank window, so the 16-byte slots
+// (address / 16 mod 32) that those lanes touch must be distinct: with a row stride of 18
+// (K) or 10 (V^T) slots, the 16 rows times 2 column chunks of a half-wavefront land on 32
+// distinct slots (the odd strides 17 and 9 give two-way conflicts on every read).
+// Workgroups are dealt to the 8 XCDs round-robin; the (head, query tile) order is remapped
+// so that each XCD runs a contiguous range of heads, whose K/V tiles then stay in its L2.
 // Softmax terms use the hardware v_exp_f32; results below 2^-126 flush to zero, which no
 // sum holding its max term can notice.  The running reference max of each query is moved
 // (and O and the sum rescaled) only when a tile's max exceeds it by more than 2^8, so exp
@@ -40,8 +50,8 @@ __global__ __launch_bounds__(256 * SPLIT, SB && SPLIT == 1 ? 3 : 1) void k_atten
                                                    uint16_t* __restrict__ out, int L, int Ls,
                                                    int H, int Hkv, float scale_log2) {
   constexpr int KT = 64;          // keys per tile
-  constexpr int LDKS = HD + 8;    // padded LDS rows
-  constexpr int LDVS = KT + 8;
+  constexpr int LDKS = HD + 16;   // padded LDS rows
+  constexpr int LDVS = KT + 16;
   constexpr int CK = KT * HD / 8 / 256;  // 16-byte chunks per thread per tile (K and V^T each)
   constexpr int NB = SB ? 1 : 2;  // LDS tile buffers
   // K tiles [NB][SPLIT][KT * LDKS], then V^T tiles [NB][SPLIT][HD * LDVS], in one region
@@ -55,8 +65,11 @@ __global__ __launch_bounds__(256 * SPLIT, SB && SPLIT == 1 ? 3 : 1) void k_atten
   // which part of the key range (wave-uniform, so tile indices and branches stay scalar)
   const int part = __builtin_amdgcn_readfirstlane(wave >> 2);
   const int tl = tid & 255, tpart = part;    // loader thread: its index and part
-  const int bh = blockIdx.y, b = bh / H, h = bh % H, kvh = h / (H / Hkv);
-  const int q0 = blockIdx.x * 64 + (wave & 3) * 16;
+  // (head, query tile) of this workgroup: contiguous ranges per XCD
+  const int li = xcd_remap(blockIdx.x + blockIdx.y * gridDim.x, gridDim.x * gridDim.y);
+  const int qt = li % gridDim.x, bh = li / gridDim.x;
+  const int b = bh / H, h = bh % H, kvh = h / (H / Hkv);
+  const int q0 = qt * 64 + (wave & 3) * 16;
   const int g = lane >> 4, r16 = lane & 15;
 
   const uint16_t* qh = q + ((int64_t)(b * H + h) * Ls) * HD;
@@ -127,17 +140,34 @@ __global__ __launch_bounds__(256 * SPLIT, SB && SPLIT == 1 ? 3 : 1) void k_atten
     const int next = tpart * per + j + 1;  // this thread's next tile to load
     if (j + 1 < per && next < n_tiles) fetch(next * KT);  // in flight during this tile
     if (kt < n_tiles) {
+      // K fragments are requested in two batches of 8 (two 16-key blocks each), each
+      // batch before its MFMAs: two LDS round trips per tile, in 32 registers
       f32x4_t st[4];
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
-        st[kb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      for (int hb = 0; hb < 2; ++hb) {
+        bf16x8_t kf[2][HD / 32];
 #pragma unroll
-        for (int kk = 0; kk < HD / 32; ++kk) {
-          const bf16x8_t a = as_bf16x8(
-              *reinterpret_cast<const u32x4_t*>(Kt(buf, part) + (kb * 16 + r16) * LDKS + kk * 32 + g * 8));
-          st[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[kk], st[kb], 0, 0, 0);
-        }
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int kk = 0; kk < HD / 32; ++kk)
+            kf[kb][kk] = as_bf16x8(*reinterpret_cast<const u32x4_t*>(
+                Kt(buf, part) + ((2 * hb + kb) * 16 + r16) * LDKS + kk * 32 + g * 8));
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) st[2 * hb + kb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kk = 0; kk < HD / 32; ++kk)
+#pragma unroll
+          for (int kb = 0; kb < 2; ++kb)
+            st[2 * hb + kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[kb][kk], qf[kk], st[2 * hb + kb], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
       }
+      // the first key step's V^T fragments are requested before the softmax
+      u32x4_t vf[HD / 16];
+#pragma unroll
+      for (int d = 0; d < HD / 16; ++d)
+        vf[d] = *reinterpret_cast<const u32x4_t*>(Vt(buf, part) + (d * 16 + r16) * LDVS + g * 8);
+      __builtin_amdgcn_sched_barrier(0);
       if (key0 + KT > L) {  // partial last tile (scalar branch): keys past L drop out
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb)
@@ -147,16 +177,18 @@ __global__ __launch_bounds__(256 * SPLIT, SB && SPLIT == 1 ? 3 : 1) void k_atten
             if (key >= L) st[kb][i] = -INFINITY;
           }
       }
-      float tmax = -INFINITY;  // raw scores: the scale is positive
+      float lmax = -INFINITY;  // this lane's max of raw scores (the scale is positive)
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) tmax = fmaxf(tmax, st[kb][i]);
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-      const float tm = tmax * scale_log2;
-      const bool grow = tm > m_ref + SLACK;  // true on a lane's first tile (m_ref = -inf)
-      if (__any(grow)) {
+        for (int i = 0; i < 4; ++i) lmax = fmaxf(lmax, st[kb][i]);
+      // the lane groups of a query exchange their maxima only when some lane holds a score
+      // beyond its query's reference by more than SLACK; otherwise no reference moves
+      if (__any(lmax * scale_log2 > m_ref + SLACK)) {
+        float tmax = fmaxf(lmax, __shfl_xor(lmax, 16, 64));
+        tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+        const float tm = tmax * scale_log2;
+        const bool grow = tm > m_ref + SLACK;  // true on a lane's first tile (m_ref = -inf)
         const float m_new = grow ? tm : m_ref;
         const float alpha = fast_exp2(m_ref - m_new);  // 1 where kept, 0 while m_ref is -inf
         m_ref = m_new;
@@ -180,12 +212,16 @@ __global__ __launch_bounds__(256 * SPLIT, SB && SPLIT == 1 ? 3 : 1) void k_atten
         pb.z = pack_bf16x2(st[2 * ks + 1][0], st[2 * ks + 1][1]);
         pb.w = pack_bf16x2(st[2 * ks + 1][2], st[2 * ks + 1][3]);
         const bf16x8_t bfrag = as_bf16x8(pb);
+        if (ks == 1) {
 #pragma unroll
-        for (int d = 0; d < HD / 16; ++d) {
-          const u32x4_t av = *reinterpret_cast<const u32x4_t*>(
-              Vt(buf, part) + (d * 16 + r16) * LDVS + ks * 32 + g * 8);
-          o[d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(av), bfrag, o[d], 0, 0, 0);
+          for (int d = 0; d < HD / 16; ++d)
+            vf[d] = *reinterpret_cast<const u32x4_t*>(Vt(buf, part) + (d * 16 + r16) * LDVS + 32 + g * 8);
+          __builtin_amdgcn_sched_barrier(0);
         }
+#pragma unroll
+        for (int d = 0; d < HD / 16; ++d)
+          o[d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vf[d]), bfrag, o[d], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
     if (j + 1 < per) {
