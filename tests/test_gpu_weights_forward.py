@@ -86,6 +86,16 @@ def test_gqa_bias_forward(spec):
     _check_logits(spec, 2, 100, 10, 40)
 
 
+@pytest.mark.parametrize("B,L,row_begin,n_rows", [(1, 40, 0, 40), (3, 200, 150, 50), (64, 300, 100, 40)])
+def test_hd128_attention_paths(B, L, row_begin, n_rows):
+    """hd 128 attention, the direct-to-LDS kernel: L = 40 is one key tile, so the second
+    key-range part of the small-grid launch has no tile and merges an empty state; L = 200
+    splits 4 tiles over two parts, the last one partial; B = 64, L = 300 has 640 query-tile
+    workgroups and takes the one-part launch, again with a partial last tile."""
+    require_gpu()
+    _check_logits(MINI_HD128, B, L, row_begin, n_rows)
+
+
 @pytest.mark.parametrize("B,L,row_begin,n_rows", [(2, 130, 60, 40), (1, 256, 128, 32)])
 def test_split_k_forward(B, L, row_begin, n_rows):
     """L = 130: row groups of 4 straddle two sequences (per-row v path); L = 256: vector v."""
