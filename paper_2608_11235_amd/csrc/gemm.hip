@@ -97,7 +97,7 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void k_gemm(GemmArgs g) {
   constexpr int NACC = TM * TN * 16;    // accumulators per thread
   static_assert(NT % 8 == 0, "threads must cover whole 64-element rows");
   static_assert(EPI != EPI_SWIGLU || TN % 2 == 0, "SwiGLU epilogue pairs 32-column blocks");
-  static_assert(PIPE != 2 || TM * TN == 4, "PIPE 2 schedules 4 MFMAs per k-step");
+  static_assert(PIPE != 2 || TM * TN == 4 || TM * TN == 2, "PIPE 2 schedules 4 or 2 MFMAs per k-step");
 
   // PIPE 2 stores every thread's chunks unconditionally: rows past the tile land in spare
   // LDS rows (CA * NT / 8 >= BM)
@@ -254,22 +254,22 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void k_gemm(GemmArgs g) {
     load_frags(cur, 16, fa1, fb1);                                                      \
     mfmas(fa0, fb0);                                                                    \
     stash_a(cur ^ 1, RAN);                                                              \
-    _Pragma("unroll") for (int q = 0; q < 4; ++q) { SG(0x008, 1); SG(0x100, 1); SG(0x200, 1); } \
+    _Pragma("unroll") for (int q = 0; q < TM * TN; ++q) { SG(0x008, 1); SG(0x100, 1); SG(0x200, 1); } \
     __builtin_amdgcn_sched_barrier(0);                                                  \
     load_frags(cur, 32, fa0, fb0);                                                      \
     mfmas(fa1, fb1);                                                                    \
     stash_b(cur ^ 1, RBN);                                                              \
-    _Pragma("unroll") for (int q = 0; q < 4; ++q) { SG(0x008, 1); SG(0x100, 1); SG(0x200, 1); } \
+    _Pragma("unroll") for (int q = 0; q < TM * TN; ++q) { SG(0x008, 1); SG(0x100, 1); SG(0x200, 1); } \
     __builtin_amdgcn_sched_barrier(0);                                                  \
     load_frags(cur, 48, fa1, fb1);                                                      \
     mfmas(fa0, fb0);                                                                    \
     FETCH_ALL(RAN, RBN, kt_ + 3 < nk ? kt_ + 3 : nk - 1);                               \
-    _Pragma("unroll") for (int q = 0; q < 4; ++q) { SG(0x008, 1); SG(0x100, 1); SG(0x020, 2); } \
+    _Pragma("unroll") for (int q = 0; q < TM * TN; ++q) { SG(0x008, 1); SG(0x100, 1); SG(0x020, 2); } \
     __builtin_amdgcn_sched_barrier(0);                                                  \
     __syncthreads();                                                                    \
     load_frags(cur ^ 1, 0, fa0, fb0);                                                   \
     mfmas(fa1, fb1);                                                                    \
-    _Pragma("unroll") for (int q = 0; q < 4; ++q) { SG(0x008, 1); SG(0x100, 1); }       \
+    _Pragma("unroll") for (int q = 0; q < TM * TN; ++q) { SG(0x008, 1); SG(0x100, 1); }       \
     __builtin_amdgcn_sched_barrier(0);                                                  \
   } while (0)
     FETCH_ALL(ra0, rb0, 0);
@@ -590,8 +590,11 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void k_gemm(GemmArgs g) {
 // cfg 1:  32 x 128 tile, 4 waves (1 x 4) (2 waves for SwiGLU), for M <= 64 (LM head rows)
 // cfg 2: 256 x 128 tile,  8 waves (4 x 2), wave tile 64 x 64, PIPE 2
 // cfg 3: 256 x 192 tile, 12 waves (4 x 3), wave tile 64 x 64, PIPE 2
-// cfg 4: 128 x 192 tile,  6 waves (2 x 3), wave tile 64 x 64, PIPE 2: twice the tiles of
-//        cfg 3, so an output of 512 rows x 12288 columns fills 256 CUs without splitting K
+// cfg 4: 128 x 192 tile, 12 waves (4 x 3), wave tile 32 x 64, PIPE 2: twice the tiles of
+//        cfg 3, so an output of 512 rows x 12288 columns fills 256 CUs without splitting K.
+//        Twelve waves load the four SIMDs evenly (three each); as 6 waves of 64 x 64 (two
+//        SIMDs with two waves, two with one) the QKV projection at 512 rows ran 1.2 %
+//        slower per pass, although a 32 x 64 wave tile reads 1.5 x the LDS bytes per MFMA
 struct CfgShape { int bm, bn; };
 static CfgShape cfg_shape(int cfg) {
   switch (cfg) {
@@ -612,9 +615,10 @@ int gemm_top1_parts(const GemmPlan& p, int N) {
   return (N + sh.bn - 1) / sh.bn * waves_n;
 }
 
-// Relative main-loop efficiency of the large-tile configs (16, 12, 8 and 6 waves per
+// Relative main-loop efficiency of the large-tile configs (16, 12, 8 and 12 waves per
 // workgroup), measured on the pass's shapes (cfg 4: 64.4 us for the whole-K QKV projection
-// with its bias + RoPE epilogue at 512 x 12288 x 4096).
+// with its bias + RoPE epilogue at 512 x 12288 x 4096, as 6 waves; the 12-wave layout is a
+// few us faster there, and keeping the 6-wave figure leaves every plan as it was).
 static double cfg_eff(int cfg) {
   return cfg == 0 ? 1.0 : (cfg == 3 ? 1.03 : (cfg == 4 ? 0.72 : 0.88));
 }
@@ -699,7 +703,7 @@ static hipError_t run_cfg(int cfg, const GemmArgs& a, int grid, hipStream_t s, h
       if constexpr (EPI == EPI_SWIGLU) return run<1, 2, 1, 2, EPI, 1>(a, grid, s, e0, e1);
       else return run<1, 4, 1, 1, EPI, 1>(a, grid, s, e0, e1);
     case 3: return run<4, 3, 2, 2, EPI, 2>(a, grid, s, e0, e1);
-    case 4: return run<2, 3, 2, 2, EPI, 2>(a, grid, s, e0, e1);
+    case 4: return run<4, 3, 1, 2, EPI, 2>(a, grid, s, e0, e1);
     default: return run<4, 2, 2, 2, EPI, 2>(a, grid, s, e0, e1);
   }
 }
