@@ -5,9 +5,10 @@
 // One workgroup = 64 queries of one head (4 wavefronts x 16 queries) times SPLIT parts of
 // the key range: with SPLIT = 2 a second group of 4 wavefronts runs the same queries over
 // the second half of the key tiles, and the partial softmax states (max, sum, O) are merged
-// through LDS at the end, in part order.  Small grids (at most two workgroups per CU for
-// the model's max_batch: the choice is made for the rows a launch is planned for, not the
-// live ones, so that a row's rounding never depends on its batch) use SPLIT = 2.
+// through LDS at the end, in part order.  Small grids use SPLIT = 2: at most two
+// workgroups per CU at hd 128, fewer than two at hd 64, counted for the model's max_batch
+// (the choice is made for the rows a launch is planned for, not the live ones, so that a
+// row's rounding never depends on its batch).
 // Two kernels share the arithmetic:
 //  - k_attention_dl (hd 128, the model shapes) fetches the 64-key K and V^T tiles straight
 //    into LDS with 16-byte buffer loads that write LDS (no staging registers), which keeps
